@@ -1,0 +1,279 @@
+"""Pins for the fp64 oracle: closed forms, invariants, finite differences, a
+naive second evaluation and a library routine. None of these re-types the
+oracle's formulas; each would fail on a plausible mistake in it (a dropped
+scale, a wrong sign, a transposed operand, a missing D term, a log base)."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import attention as A
+import workloads
+
+
+def rand(rng, *shape, sigma=1.0):
+    return rng.standard_normal(shape) * sigma
+
+
+def loss(q, k, v, dout, s):
+    o, _ = oracle.forward(q, k, v, s)
+    return float(np.sum(dout * o))
+
+
+# ---------------------------------------------------------------- closed forms
+
+
+def test_identical_keys_give_mean_of_v():
+    rng = np.random.default_rng(1)
+    B, H, N, d = 2, 3, 37, 16
+    q = rand(rng, B, H, N, d)
+    k = np.broadcast_to(rand(rng, B, H, 1, d), (B, H, N, d)).copy()
+    v = rand(rng, B, H, N, d)
+    dout = rand(rng, B, H, N, d)
+    s = 0.25
+    r = oracle.forward_backward(q, k, v, dout, s)
+    np.testing.assert_allclose(r["o"], np.broadcast_to(v.mean(axis=2, keepdims=True), v.shape), atol=1e-13)
+    lse_expected = s * np.einsum("bhnd,bhd->bhn", q, k[:, :, 0]) + math.log(N)
+    np.testing.assert_allclose(r["lse"], lse_expected, atol=1e-12)
+    # every row of dS sums to zero and all keys are equal, so dQ = s * k * 0
+    assert np.abs(r["dq"]).max() < 1e-12
+
+
+def test_dominant_key_returns_its_value_row():
+    rng = np.random.default_rng(2)
+    N, d = 50, 8
+    q = rand(rng, 1, 1, N, d)
+    k = rand(rng, 1, 1, N, d) * 0.01
+    jstar = 17
+    # make s*q_i.(k_j* - k_j) >= 40 for every i and j != j*
+    q[..., 0] = np.abs(q[..., 0]) + 1.0
+    q[..., 1:] = 0.0
+    k[0, 0, jstar, 0] = 200.0
+    v = rand(rng, 1, 1, N, d)
+    o, lse = oracle.forward(q, k, v, 1.0)
+    np.testing.assert_allclose(o[0, 0], np.broadcast_to(v[0, 0, jstar], (N, d)), rtol=0, atol=1e-15)
+    np.testing.assert_allclose(lse[0, 0], q[0, 0, :, 0] * 200.0, rtol=1e-15)
+
+
+def test_single_token():
+    rng = np.random.default_rng(3)
+    q, k, v, dout = (rand(rng, 1, 2, 1, 8) for _ in range(4))
+    s = 0.3125
+    r = oracle.forward_backward(q, k, v, dout, s)
+    np.testing.assert_allclose(r["o"], v, rtol=1e-15)
+    np.testing.assert_allclose(r["lse"], s * np.sum(q * k, axis=-1), rtol=1e-14)
+    assert np.abs(r["dq"]).max() < 1e-15 and np.abs(r["dk"]).max() < 1e-15
+    np.testing.assert_allclose(r["dv"], dout, rtol=1e-15)
+
+
+def test_all_ones_v_rows_of_p_sum_to_one():
+    rng = np.random.default_rng(4)
+    q, k = rand(rng, 1, 2, 70, 16, sigma=3.0), rand(rng, 1, 2, 70, 16, sigma=3.0)
+    o, _ = oracle.forward(q, k, np.ones((1, 2, 70, 5)), 0.25)
+    assert np.abs(o - 1.0).max() <= 1e-12
+
+
+def test_identity_v_exposes_probabilities():
+    # with V = I (N = d), O = P: nonnegative, rows sum to 1, and P_ij / P_ik = exp(s q_i.(k_j - k_k))
+    rng = np.random.default_rng(5)
+    N = 12
+    q, k = rand(rng, 1, 1, N, N), rand(rng, 1, 1, N, N)
+    s = 0.4375
+    P, _ = oracle.forward(q, k, np.eye(N)[None, None], s)
+    P = P[0, 0]
+    assert P.min() > 0
+    assert np.abs(P.sum(axis=1) - 1).max() < 1e-14
+    ratio = P[:, 3] / P[:, 7]
+    np.testing.assert_allclose(ratio, np.exp(s * q[0, 0] @ (k[0, 0, 3] - k[0, 0, 7])), rtol=1e-12)
+
+
+# ----------------------------------------------------------------- invariants
+
+
+def test_token_permutation_equivariance():
+    rng = np.random.default_rng(6)
+    B, H, N, d = 1, 2, 45, 8
+    q, k, v, dout = (rand(rng, B, H, N, d) for _ in range(4))
+    s = 0.375
+    pi = rng.permutation(N)
+    r = oracle.forward_backward(q, k, v, dout, s)
+    rp = oracle.forward_backward(q[:, :, pi], k[:, :, pi], v[:, :, pi], dout[:, :, pi], s)
+    for name in ("o", "lse", "dq", "dk", "dv"):
+        np.testing.assert_allclose(rp[name], r[name][:, :, pi], rtol=1e-11, atol=1e-13)
+    # permuting only the key/value pairs leaves O and LSE unchanged
+    o2, lse2 = oracle.forward(q, k[:, :, pi], v[:, :, pi], s)
+    np.testing.assert_allclose(o2, r["o"], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(lse2, r["lse"], rtol=1e-13)
+
+
+def test_linearity_in_v_and_head_independence():
+    rng = np.random.default_rng(7)
+    B, H, N, d = 2, 3, 33, 8
+    q, k, v, v2 = (rand(rng, B, H, N, d) for _ in range(4))
+    s = 0.5
+    o1, _ = oracle.forward(q, k, v, s)
+    o2, _ = oracle.forward(q, k, v2, s)
+    o3, _ = oracle.forward(q, k, 2.5 * v - 0.75 * v2, s)
+    np.testing.assert_allclose(o3, 2.5 * o1 - 0.75 * o2, atol=1e-12)
+    for b in range(B):
+        for h in range(H):
+            oh, _ = oracle.forward(q[b:b + 1, h:h + 1], k[b:b + 1, h:h + 1], v[b:b + 1, h:h + 1], s)
+            np.testing.assert_array_equal(oh[0, 0], o1[b, h])
+
+
+def test_gradient_identities():
+    rng = np.random.default_rng(8)
+    B, H, N, d = 1, 2, 200, 16
+    q, k, v, dout = (rand(rng, B, H, N, d) for _ in range(4))
+    q[:, 0] *= 4
+    k[:, 0] *= 4
+    r = oracle.forward_backward(q, k, v, dout, 0.25)
+    assert np.abs(r["dk"].sum(axis=2)).max() < 1e-11
+    np.testing.assert_allclose(r["dv"].sum(axis=2), dout.sum(axis=2), atol=1e-11)
+    np.testing.assert_allclose(np.sum(q * r["dq"], axis=(2, 3)), np.sum(k * r["dk"], axis=(2, 3)), rtol=1e-10)
+    np.testing.assert_allclose(np.sum(v * r["dv"], axis=(2, 3)), np.sum(r["o"] * dout, axis=(2, 3)), rtol=1e-10)
+
+
+def test_blocking_does_not_change_results():
+    rng = np.random.default_rng(9)
+    q, k, v, dout = (rand(rng, 1, 2, 101, 8) for _ in range(4))
+    r1 = oracle.forward_backward(q, k, v, dout, 0.3125, block=512)
+    r2 = oracle.forward_backward(q, k, v, dout, 0.3125, block=7)
+    for name in r1:
+        np.testing.assert_allclose(r2[name], r1[name], rtol=1e-12, atol=1e-14)
+
+
+# ------------------------------------------- independent evaluations of the definition
+
+
+@pytest.mark.parametrize("N,d", [(1, 3), (5, 4), (13, 6)])
+def test_blocked_matches_naive_loops(N, d):
+    rng = np.random.default_rng(10 + N)
+    q, k, v, dout = (rand(rng, 1, 1, N, d) for _ in range(4))
+    s = 0.6875
+    r = oracle.forward_backward(q, k, v, dout, s, block=4)
+    n = oracle.naive.attention_head(q[0, 0].tolist(), k[0, 0].tolist(), v[0, 0].tolist(), s, dout[0, 0].tolist())
+    for name in ("o", "lse", "D", "dq", "dk", "dv"):
+        np.testing.assert_allclose(r[name][0, 0], np.array(n[name]), rtol=1e-12, atol=1e-14)
+
+
+def test_gradients_match_central_finite_differences():
+    rng = np.random.default_rng(11)
+    N, d = 9, 4
+    q, k, v, dout = (rand(rng, 1, 1, N, d) for _ in range(4))
+    s = 0.8125
+    r = oracle.forward_backward(q, k, v, dout, s)
+    h = 1e-6
+    for name, x in (("dq", q), ("dk", k), ("dv", v)):
+        g = np.empty_like(x)
+        for idx in np.ndindex(x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += h
+            xm[idx] -= h
+            args_p = {"q": q, "k": k, "v": v}
+            args_m = dict(args_p)
+            args_p[name[1]] = xp
+            args_m[name[1]] = xm
+            g[idx] = (loss(args_p["q"], args_p["k"], args_p["v"], dout, s)
+                      - loss(args_m["q"], args_m["k"], args_m["v"], dout, s)) / (2 * h)
+        err = np.abs(g - r[name]).max() / np.abs(r[name]).max()
+        assert err < 1e-7, (name, err)
+
+
+def test_matches_torch_sdpa_with_autograd():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(12)
+    B, H, N, d = 2, 3, 77, 16
+    q, k, v, dout = (rand(rng, B, H, N, d, sigma=2.0) for _ in range(4))
+    s = 0.25
+    r = oracle.forward_backward(q, k, v, dout, s, block=32)
+    tq, tk, tv = (torch.tensor(x, requires_grad=True) for x in (q, k, v))
+    to = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, scale=s)
+    to.backward(torch.tensor(dout))
+    np.testing.assert_allclose(r["o"], to.detach().numpy(), rtol=1e-11, atol=1e-13)
+    for name, t in (("dq", tq), ("dk", tk), ("dv", tv)):
+        np.testing.assert_allclose(r[name], t.grad.numpy(), rtol=1e-10, atol=1e-12)
+    lse_t = torch.logsumexp(s * torch.tensor(q) @ torch.tensor(k).transpose(-1, -2), dim=-1)
+    np.testing.assert_allclose(r["lse"], lse_t.numpy(), rtol=1e-13)
+
+
+# ------------------------------------------------------------ sampled-row paths
+
+
+def test_query_rows_and_key_rows_match_full_pass():
+    rng = np.random.default_rng(13)
+    B, H, N, d = 2, 2, 150, 8
+    bits = {n: workloads.random_bf16(rng, (B, H, N, d)) for n in ("q", "k", "v", "dout")}
+    s = 1 / math.sqrt(8)
+    full = oracle.forward_backward(bits["q"], bits["k"], bits["v"], bits["dout"], s)
+    rows = np.array([[0, 0, 0], [0, 1, 149], [1, 0, 77], [1, 1, 3], [1, 1, 100]])
+    qr = oracle.query_rows(bits["q"], bits["k"], bits["v"], s, rows, dout=bits["dout"])
+    for name in ("o", "lse", "D", "dq"):
+        np.testing.assert_allclose(qr[name], full[name][rows[:, 0], rows[:, 1], rows[:, 2]], rtol=1e-12,
+                                   atol=1e-14)
+    keys = np.array([0, 5, 149])
+    lse, D = oracle.row_statistics(bits["q"], bits["k"], bits["v"], bits["dout"], s, 1, 0)
+    np.testing.assert_allclose(lse, full["lse"][1, 0], rtol=1e-14)
+    dk, dv = oracle.key_rows(bits["q"], bits["k"], bits["v"], bits["dout"], s, 1, 0, keys, lse, D, block=64)
+    np.testing.assert_allclose(dk, full["dk"][1, 0, keys], rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(dv, full["dv"][1, 0, keys], rtol=1e-11, atol=1e-13)
+
+
+def test_bf16_decode_is_exact():
+    bits = np.array([0x0000, 0x8000, 0x3F80, 0xBF80, 0x4049, 0x7F7F, 0x0001], dtype=np.uint16)
+    expected = [0.0, -0.0, 1.0, -1.0, 3.140625, 3.3895313892515355e38, 9.183549615799121e-41]
+    np.testing.assert_array_equal(oracle.decode_bf16(bits), np.array(expected))
+
+
+def test_scale_is_rounded_to_fp32():
+    assert oracle.fp32_scale(1 / math.sqrt(128)) == 0.08838834613561630
+    assert oracle.fp32_scale(0.125) == 0.125
+
+
+# ------------------------------- the pins catch planted mistakes in the oracle
+
+
+def _fd_error(block_backward, which):
+    rng = np.random.default_rng(14)
+    N, d = 6, 3
+    q, k, v, dout = (rand(rng, 1, 1, N, d) for _ in range(4))
+    s = 0.875
+    r = block_backward(q[0, 0], k[0, 0], v[0, 0], dout[0, 0], s)
+    grad = {"dq": r["dq"], "dk": r["dk_part"], "dv": r["dv_part"]}[which]
+    x = {"dq": q, "dk": k, "dv": v}[which]
+    h = 1e-6
+    g = np.empty_like(x)
+    for idx in np.ndindex(x.shape):
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += h
+        xm[idx] -= h
+        args_p = {"q": q, "k": k, "v": v}
+        args_m = dict(args_p)
+        args_p[which[1]] = xp
+        args_m[which[1]] = xm
+        g[idx] = (loss(args_p["q"], args_p["k"], args_p["v"], dout, s)
+                  - loss(args_m["q"], args_m["k"], args_m["v"], dout, s)) / (2 * h)
+    return np.abs(g[0, 0] - grad).max() / np.abs(g).max()
+
+
+def _mutant(kind):
+    def bb(qb, K, V, dOb, s):
+        _, lse, P, O = A._block_forward(qb, K, V, s)
+        dP = dOb @ V.T
+        D = np.einsum("ic,ic->i", dOb, O)
+        if kind == "no_D":
+            D = 0 * D
+        dS = P * (dP - D[:, None]) if kind != "sign" else P * (D[:, None] - dP)
+        dk = s * (dS.T @ qb) if kind != "dk_no_scale" else dS.T @ qb
+        dv = P.T @ dOb if kind != "dv_transposed" else (P @ dOb if P.shape[0] == P.shape[1] else None)
+        return {"dq": s * (dS @ K), "dk_part": dk, "dv_part": dv}
+
+    return bb
+
+
+@pytest.mark.parametrize("kind,which", [("no_D", "dq"), ("sign", "dk"), ("dk_no_scale", "dk"),
+                                        ("dv_transposed", "dv")])
+def test_finite_difference_pin_rejects_planted_mistakes(kind, which):
+    assert _fd_error(A._block_backward, which) < 1e-7
+    assert _fd_error(_mutant(kind), which) > 1e-3
