@@ -1,0 +1,120 @@
+/*
+ * vitattn.h — C ABI of the exact non-causal attention library for MI355X (gfx950).
+ *
+ * What it computes. One GPU's share of the self-attention of a long-sequence
+ * Vision Transformer after a DeepSpeed-Ulysses all-to-all (paper Sec. II-E):
+ * the full sequence of N patch tokens for H heads of B samples. Attention is
+ * dense and bidirectional: every token attends to every token (Sec. I and III),
+ * with no mask, bias or dropout. Per (b, h), with s = scale:
+ *
+ *     S = s Q K^T,  LSE_i = log sum_j exp(S_ij),  P = exp(S - LSE 1^T),  O = P V
+ *
+ * and the backward pass, given dO = dL/dO:
+ *
+ *     D_i = sum_c dO_ic O_ic,  dS = P o (dO V^T - D 1^T),
+ *     dQ = s dS K,  dK = s dS^T Q,  dV = P^T dO.
+ *
+ * The tiling (the N x N matrices S and P are never stored), the saved per-row
+ * logsumexp and the recomputation of P in the backward pass follow
+ * FlashAttention-2, which the paper uses (Sec. II-F, V-B, V-E).
+ *
+ * Conventions shared by every entry point:
+ *  - All tensor pointers are DEVICE pointers owned by the caller. The library
+ *    never allocates, frees or retains them, and holds no per-call state.
+ *  - Tensors are contiguous row-major [B][H][N][d] (d innermost); lse and the
+ *    backward workspace are [B][H][N]. Element offsets use 64-bit arithmetic.
+ *  - q, k, v and dout hold bfloat16 values as raw 16-bit patterns. o, lse, dq,
+ *    dk and dv are fp32. Every pointer must be 16-byte aligned.
+ *  - Supported head dims: d = 64 and d = 128. Any N >= 1.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *    the call returns without waiting. Execution faults surface at the
+ *    caller's next synchronisation on that stream.
+ *  - Arguments are validated before anything is launched; on any error status
+ *    no output is written and no kernel is enqueued. Validation itself makes
+ *    no HIP call, so it works on a machine without a GPU.
+ *  - Results are bitwise deterministic for identical inputs (no atomics).
+ *  - Calls are thread-safe; concurrent calls on different streams are fine.
+ */
+#ifndef VITATTN_H
+#define VITATTN_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum vitattn_status {
+  VITATTN_OK = 0,
+  VITATTN_E_INVAL = 1,       /* null/misaligned pointer, B/H/N < 1, non-finite or non-positive scale, size overflow */
+  VITATTN_E_UNSUPPORTED = 2, /* d not in {64, 128} */
+  VITATTN_E_WORKSPACE = 3,   /* workspace missing or smaller than vitattn_bwd_workspace_bytes() */
+  VITATTN_E_HIP = 4,         /* the HIP runtime reported an error when launching */
+  VITATTN_E_INTERNAL = 5     /* unexpected internal failure */
+};
+
+/*
+ * Forward pass (the tiled online softmax of FlashAttention-2, cited in paper
+ * Sec. II-F).
+ *   q, k, v : bf16 [B][H][N][d], read only.
+ *   o       : fp32 [B][H][N][d], written: O = softmax(scale * Q K^T) V.
+ *   lse     : fp32 [B][H][N], written: natural-log logsumexp of each row of
+ *             the scaled logits, LSE_i = log sum_j exp(scale * q_i . k_j).
+ *   scale   : softmax scale, finite and > 0 (typically 1/sqrt(d)).
+ * Returns a vitattn_status.
+ */
+int vitattn_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int N, int d,
+                float scale, void* stream);
+
+/*
+ * Bytes of device workspace vitattn_bwd needs: 4*B*H*N (the fp32 row
+ * statistic D) rounded up to 256. Returns 0 for invalid sizes.
+ */
+size_t vitattn_bwd_workspace_bytes(int B, int H, int N, int d);
+
+/*
+ * Backward pass: a D = rowsum(dO o O) preprocess, then one kernel that
+ * accumulates dK and dV per key block and one that accumulates dQ per query
+ * block, both recomputing P from q, k and lse (FlashAttention-2's backward,
+ * cited in paper Sec. II-F).
+ *   q, k, v   : bf16 [B][H][N][d], the forward inputs.
+ *   o, lse    : fp32, the forward outputs of vitattn_fwd for the same inputs.
+ *   dout      : bf16 [B][H][N][d], the gradient of the loss with respect to o.
+ *   dq, dk, dv: fp32 [B][H][N][d], written.
+ *   workspace : device buffer of at least vitattn_bwd_workspace_bytes() bytes,
+ *               overwritten; it must not alias any other argument.
+ * Returns a vitattn_status.
+ */
+int vitattn_bwd(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
+                float* dq, float* dk, float* dv, int B, int H, int N, int d, float scale, void* workspace,
+                size_t workspace_bytes, void* stream);
+
+/*
+ * The three stages of vitattn_bwd, callable one by one (same arguments,
+ * layouts and validation as vitattn_bwd; used to time each kernel). They
+ * must run in this order on one stream, all with the same workspace:
+ *   vitattn_bwd_rowdot: workspace <- D_i = sum_c dout_ic o_ic  (fp32 [B][H][N]);
+ *   vitattn_bwd_dkdv  : dk, dv from q, k, v, dout, lse and D in the workspace;
+ *   vitattn_bwd_dq    : dq from q, k, v, dout, lse and D in the workspace.
+ * Each stage validates its own arguments like vitattn_bwd does.
+ */
+int vitattn_bwd_rowdot(const float* o, const void* dout, int B, int H, int N, int d, void* workspace,
+                       size_t workspace_bytes, void* stream);
+int vitattn_bwd_dkdv(const void* q, const void* k, const void* v, const void* dout, const float* lse, float* dk,
+                     float* dv, int B, int H, int N, int d, float scale, const void* workspace,
+                     size_t workspace_bytes, void* stream);
+int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout, const float* lse, float* dq,
+                   int B, int H, int N, int d, float scale, const void* workspace, size_t workspace_bytes,
+                   void* stream);
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* vitattn_status_str(int status);
+
+/* Library version string (static storage). */
+const char* vitattn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VITATTN_H */

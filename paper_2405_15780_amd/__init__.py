@@ -1,0 +1,21 @@
+"""Exact non-causal multi-head attention (forward and backward) for MI355X.
+
+A thin ctypes binding over the C ABI in include/vitattn.h; it only marshals
+arguments. Every step of the computation runs in the library's HIP kernels.
+PyTorch is used for device memory and the current stream only. If the built
+library is missing the import of a binding function raises: there is no
+fallback path.
+"""
+from .binding import (  # noqa: F401
+    LIB_PATH,
+    VitattnError,
+    bwd,
+    bwd_dkdv,
+    bwd_dq,
+    bwd_rowdot,
+    fwd,
+    library,
+    status_str,
+    version,
+    workspace_bytes,
+)

@@ -1,0 +1,157 @@
+"""ctypes binding of libvitattn.so (argument marshalling only).
+
+Raw entry points (`library().vitattn_fwd(...)` etc.) take integer device
+pointers exactly like the C ABI. The tensor helpers below allocate outputs
+with PyTorch, pass `data_ptr()`s and the current HIP stream, and raise
+VitattnError on a non-zero status.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import threading
+
+from ._build import LIB_PATH
+
+_lock = threading.Lock()
+_lib = None
+
+c_int, c_float, c_size_t, c_void_p = ctypes.c_int, ctypes.c_float, ctypes.c_size_t, ctypes.c_void_p
+
+_SIGNATURES = {
+    "vitattn_fwd": (c_int, [c_void_p] * 5 + [c_int] * 4 + [c_float, c_void_p]),
+    "vitattn_bwd_workspace_bytes": (c_size_t, [c_int] * 4),
+    "vitattn_bwd": (c_int, [c_void_p] * 9 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
+    "vitattn_bwd_rowdot": (c_int, [c_void_p] * 2 + [c_int] * 4 + [c_void_p, c_size_t, c_void_p]),
+    "vitattn_bwd_dkdv": (c_int, [c_void_p] * 7 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
+    "vitattn_bwd_dq": (c_int, [c_void_p] * 6 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
+    "vitattn_status_str": (ctypes.c_char_p, [c_int]),
+    "vitattn_version": (ctypes.c_char_p, []),
+}
+
+
+class VitattnError(RuntimeError):
+    def __init__(self, status: int):
+        self.status = status
+        super().__init__(status_str(status))
+
+
+def library():
+    """Load libvitattn.so once. Raises if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise ImportError(f"{LIB_PATH} is missing: build it with paper_2405_15780_amd._build.build()")
+            lib = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in _SIGNATURES.items():
+                fn = getattr(lib, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = lib
+    return _lib
+
+
+def status_str(status: int) -> str:
+    return library().vitattn_status_str(status).decode()
+
+
+def version() -> str:
+    return library().vitattn_version().decode()
+
+
+def workspace_bytes(B: int, H: int, N: int, d: int) -> int:
+    return int(library().vitattn_bwd_workspace_bytes(B, H, N, d))
+
+
+def _check(status: int):
+    if status != 0:
+        raise VitattnError(status)
+
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _stream_ptr(t) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _as_input(t, name):
+    torch = _torch()
+    if not (t.is_cuda and t.dtype == torch.bfloat16 and t.dim() == 4 and t.is_contiguous()):
+        raise TypeError(f"{name} must be a contiguous 4-D bfloat16 CUDA tensor [B, H, N, d]")
+    return t
+
+
+def _default_scale(d, scale):
+    return 1.0 / math.sqrt(d) if scale is None else float(scale)
+
+
+def fwd(q, k, v, scale=None, out=None):
+    """O (fp32 [B,H,N,d]) and LSE (fp32 [B,H,N]) of softmax(scale Q K^T) V."""
+    torch = _torch()
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _as_input(t, n)
+    B, H, N, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k and v must have the same shape")
+    if out is None:
+        o = torch.empty((B, H, N, d), dtype=torch.float32, device=q.device)
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    else:
+        o, lse = out
+    _check(library().vitattn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), B, H, N, d,
+                                 _default_scale(d, scale), _stream_ptr(q)))
+    return o, lse
+
+
+def _workspace(q, workspace):
+    torch = _torch()
+    B, H, N, d = q.shape
+    need = workspace_bytes(B, H, N, d)
+    if workspace is None:
+        workspace = torch.empty(need // 4, dtype=torch.float32, device=q.device)
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None):
+    """dQ, dK, dV (fp32 [B,H,N,d]) for the upstream gradient dout (bf16)."""
+    torch = _torch()
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (dout, "dout")):
+        _as_input(t, n)
+    B, H, N, d = q.shape
+    ws, ws_bytes = _workspace(q, workspace)
+    if out is None:
+        dq, dk, dv = (torch.empty((B, H, N, d), dtype=torch.float32, device=q.device) for _ in range(3))
+    else:
+        dq, dk, dv = out
+    _check(library().vitattn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(),
+                                 lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, N, d,
+                                 _default_scale(d, scale), ws.data_ptr(), ws_bytes, _stream_ptr(q)))
+    return dq, dk, dv
+
+
+def bwd_rowdot(o, dout, workspace):
+    B, H, N, d = dout.shape
+    _check(library().vitattn_bwd_rowdot(o.data_ptr(), dout.data_ptr(), B, H, N, d, workspace.data_ptr(),
+                                        workspace.numel() * workspace.element_size(), _stream_ptr(dout)))
+
+
+def bwd_dkdv(q, k, v, dout, lse, dk, dv, workspace, scale=None):
+    B, H, N, d = q.shape
+    _check(library().vitattn_bwd_dkdv(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
+                                      dk.data_ptr(), dv.data_ptr(), B, H, N, d, _default_scale(d, scale),
+                                      workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                      _stream_ptr(q)))
+
+
+def bwd_dq(q, k, v, dout, lse, dq, workspace, scale=None):
+    B, H, N, d = q.shape
+    _check(library().vitattn_bwd_dq(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
+                                    dq.data_ptr(), B, H, N, d, _default_scale(d, scale), workspace.data_ptr(),
+                                    workspace.numel() * workspace.element_size(), _stream_ptr(q)))

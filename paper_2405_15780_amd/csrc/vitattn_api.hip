@@ -1,0 +1,181 @@
+// C ABI of the attention library: argument validation, workspace sizing and
+// status codes. Validation runs before any HIP call, so a rejected call has
+// launched nothing and written nothing, and works without a GPU.
+#include <math.h>
+#include <stdint.h>
+
+#include <exception>
+
+#include "../../include/vitattn.h"
+#include "vitattn_launch.h"
+
+#define VITATTN_VERSION "0.1.0"
+
+namespace {
+
+bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_sizes(int B, int H, int N, int d) {
+  if (B < 1 || H < 1 || N < 1) return VITATTN_E_INVAL;
+  if (d != 64 && d != 128) return VITATTN_E_UNSUPPORTED;
+  // row indices and grid sizes are 32-bit: B*H*N must fit in an int
+  const long long rows = (long long)B * H * N;
+  if (rows > 0x7fffffffLL) return VITATTN_E_INVAL;
+  return VITATTN_OK;
+}
+
+bool scale_ok(float s) { return isfinite(s) && s > 0.f; }
+
+}  // namespace
+
+extern "C" {
+
+const char* vitattn_status_str(int status) {
+  switch (status) {
+    case VITATTN_OK: return "VITATTN_OK";
+    case VITATTN_E_INVAL: return "VITATTN_E_INVAL: invalid argument";
+    case VITATTN_E_UNSUPPORTED: return "VITATTN_E_UNSUPPORTED: head dim must be 64 or 128";
+    case VITATTN_E_WORKSPACE: return "VITATTN_E_WORKSPACE: workspace missing or too small";
+    case VITATTN_E_HIP: return "VITATTN_E_HIP: HIP runtime error at launch";
+    case VITATTN_E_INTERNAL: return "VITATTN_E_INTERNAL: internal error";
+    default: return "VITATTN: unknown status";
+  }
+}
+
+const char* vitattn_version(void) { return VITATTN_VERSION; }
+
+size_t vitattn_bwd_workspace_bytes(int B, int H, int N, int d) {
+  if (check_sizes(B, H, N, d) != VITATTN_OK) return 0;
+  const size_t bytes = (size_t)B * H * N * sizeof(float);
+  return (bytes + 255) & ~(size_t)255;
+}
+
+int vitattn_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int N, int d,
+                float scale, void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
+      return VITATTN_E_INVAL;
+    if (!scale_ok(scale)) return VITATTN_E_INVAL;
+    vitattn::FwdArgs a;
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.o = o;
+    a.lse = lse;
+    a.BH = B * H;
+    a.N = N;
+    a.d = d;
+    a.scale = scale;
+    a.stream = static_cast<hipStream_t>(stream);
+    return vitattn::launch_fwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+static int check_workspace(const void* ws, size_t bytes, int B, int H, int N, int d) {
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 15u) != 0 ||
+      bytes < vitattn_bwd_workspace_bytes(B, H, N, d))
+    return VITATTN_E_WORKSPACE;
+  return VITATTN_OK;
+}
+
+static vitattn::BwdArgs bwd_args(const void* q, const void* k, const void* v, const float* o, const void* dout,
+                                 const float* lse, float* dq, float* dk, float* dv, int B, int H, int N, int d,
+                                 float scale, const void* workspace, void* stream) {
+  vitattn::BwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = o;
+  a.dout = static_cast<const uint16_t*>(dout);
+  a.lse = lse;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.drow = static_cast<float*>(const_cast<void*>(workspace));
+  a.BH = B * H;
+  a.N = N;
+  a.d = d;
+  a.scale = scale;
+  a.stream = static_cast<hipStream_t>(stream);
+  return a;
+}
+
+int vitattn_bwd(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
+                float* dq, float* dk, float* dv, int B, int H, int N, int d, float scale, void* workspace,
+                size_t workspace_bytes, void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(lse) ||
+        !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+      return VITATTN_E_INVAL;
+    if (!scale_ok(scale)) return VITATTN_E_INVAL;
+    st = check_workspace(workspace, workspace_bytes, B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    const vitattn::BwdArgs a = bwd_args(q, k, v, o, dout, lse, dq, dk, dv, B, H, N, d, scale, workspace, stream);
+    return vitattn::launch_bwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+int vitattn_bwd_rowdot(const float* o, const void* dout, int B, int H, int N, int d, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(o) || !aligned16(dout)) return VITATTN_E_INVAL;
+    st = check_workspace(workspace, workspace_bytes, B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    const vitattn::BwdArgs a = bwd_args(nullptr, nullptr, nullptr, o, dout, nullptr, nullptr, nullptr, nullptr, B, H,
+                                        N, d, 1.f, workspace, stream);
+    return vitattn::launch_bwd_rowdot(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+int vitattn_bwd_dkdv(const void* q, const void* k, const void* v, const void* dout, const float* lse, float* dk,
+                     float* dv, int B, int H, int N, int d, float scale, const void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(lse) || !aligned16(dk) ||
+        !aligned16(dv))
+      return VITATTN_E_INVAL;
+    if (!scale_ok(scale)) return VITATTN_E_INVAL;
+    st = check_workspace(workspace, workspace_bytes, B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    const vitattn::BwdArgs a =
+        bwd_args(q, k, v, nullptr, dout, lse, nullptr, dk, dv, B, H, N, d, scale, workspace, stream);
+    return vitattn::launch_bwd_dkdv(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout, const float* lse, float* dq,
+                   int B, int H, int N, int d, float scale, const void* workspace, size_t workspace_bytes,
+                   void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(lse) || !aligned16(dq))
+      return VITATTN_E_INVAL;
+    if (!scale_ok(scale)) return VITATTN_E_INVAL;
+    st = check_workspace(workspace, workspace_bytes, B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    const vitattn::BwdArgs a =
+        bwd_args(q, k, v, nullptr, dout, lse, dq, nullptr, nullptr, B, H, N, d, scale, workspace, stream);
+    return vitattn::launch_bwd_dq(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+}  // extern "C"

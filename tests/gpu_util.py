@@ -1,0 +1,74 @@
+"""Helpers for the GPU parity tests: move seeded bf16 inputs to the device,
+run the HIP path through the binding, and compare with the oracle."""
+import numpy as np
+
+# Tolerances: bf16 inputs, fp32 accumulation. O and the gradients use the
+# stated bounds; the LSE bound is derived from fp32 rounding of logits that
+# reach a few hundred nats in the stress head (ulp(300) ~ 3e-5) plus the
+# bf16 rounding of nothing (LSE uses fp32 P only).
+TOL_O_MAX = 1e-2
+TOL_O_REL = 5e-3
+TOL_GRAD_REL = 1e-2
+TOL_LSE_MAX = 2e-3
+
+
+def torch():
+    import torch as t
+
+    return t
+
+
+def to_device(bits):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(t.bfloat16).cuda()
+
+
+def run_hip(x, scale, backward=True):
+    import paper_2405_15780_amd as va
+
+    t = torch()
+    dev = {n: to_device(a) for n, a in x.items()}
+    o, lse = va.fwd(dev["q"], dev["k"], dev["v"], scale)
+    res = {"o": o, "lse": lse}
+    if backward:
+        dq, dk, dv = va.bwd(dev["q"], dev["k"], dev["v"], o, lse, dev["dout"], scale)
+        res.update(dq=dq, dk=dk, dv=dv)
+    t.cuda.synchronize()
+    return res
+
+
+def rel_l2(got, ref):
+    return float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+
+
+def assert_close(got: dict, ref: dict, names=("o", "lse", "dq", "dk", "dv"), label=""):
+    """got: numpy fp64 arrays from the GPU; ref: oracle arrays (same shapes)."""
+    report = {}
+    for n in names:
+        if n not in got:
+            continue
+        g, r = got[n], ref[n]
+        assert g.shape == r.shape, (n, g.shape, r.shape)
+        assert np.isfinite(g).all(), f"{label} {n}: non-finite values"
+        if n == "o":
+            report["o_max"] = float(np.abs(g - r).max())
+            report["o_rel"] = rel_l2(g, r)
+        elif n == "lse":
+            report["lse_max"] = float(np.abs(g - r).max())
+        elif np.linalg.norm(r) == 0.0:
+            # exact gradient is zero (e.g. N = 1): bound the absolute error
+            report[n + "_abs"] = float(np.abs(g).max())
+        else:
+            report[n + "_rel"] = rel_l2(g, r)
+    print(label, report, flush=True)
+    if "o_max" in report:
+        assert report["o_max"] <= TOL_O_MAX, (label, report)
+        assert report["o_rel"] <= TOL_O_REL, (label, report)
+    if "lse_max" in report:
+        assert report["lse_max"] <= TOL_LSE_MAX, (label, report)
+    for n in ("dq", "dk", "dv"):
+        if n + "_rel" in report:
+            assert report[n + "_rel"] <= TOL_GRAD_REL, (label, report)
+        if n + "_abs" in report:
+            assert report[n + "_abs"] <= 1e-5, (label, report)
+    return report

@@ -1,0 +1,165 @@
+"""The C ABI on the CPU: the library loads without a GPU, exports every
+function the header declares, and rejects invalid arguments before making
+any HIP call (so nothing is launched and no output is touched)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vitattn.h")
+
+va = pytest.importorskip("paper_2405_15780_amd")
+
+
+def lib():
+    try:
+        return va.library()
+    except ImportError as e:  # the library must be built before the tests run
+        pytest.fail(str(e))
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(vitattn_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert {"vitattn_fwd", "vitattn_bwd", "vitattn_bwd_workspace_bytes", "vitattn_status_str",
+            "vitattn_version"} <= set(names)
+    raw = ctypes.CDLL(va.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+def test_status_strings_and_version():
+    assert va.version() == "0.1.0"
+    for s in range(6):
+        assert va.status_str(s).startswith("VITATTN")
+    assert "unknown" in va.status_str(99)
+
+
+def test_workspace_bytes():
+    assert va.workspace_bytes(1, 2, 188416, 128) == 4 * 2 * 188416
+    assert va.workspace_bytes(1, 1, 1, 64) == 256
+    assert va.workspace_bytes(1, 1, 65, 64) == 512
+    assert va.workspace_bytes(1, 1, 0, 64) == 0
+    assert va.workspace_bytes(1, 1, 10, 96) == 0
+
+
+class Bufs:
+    """Aligned host buffers standing in for device pointers: validation must
+    reject the call before anything could dereference them."""
+
+    def __init__(self, n=4096):
+        self.arrays = [np.full(n, 7.0, dtype=np.float32) for _ in range(12)]
+        for a in self.arrays:
+            assert a.ctypes.data % 16 == 0
+
+    def p(self, i):
+        return self.arrays[i].ctypes.data
+
+    def untouched(self):
+        return all((a == 7.0).all() for a in self.arrays)
+
+
+E_INVAL, E_UNSUP, E_WS = 1, 2, 3
+
+
+def fwd(b, B=1, H=1, N=8, d=64, scale=0.125, override=None):
+    ptrs = [b.p(i) for i in range(5)]
+    if override:
+        for i, val in override.items():
+            ptrs[i] = val
+    return lib().vitattn_fwd(*ptrs, B, H, N, d, scale, None)
+
+
+@pytest.mark.parametrize("kw,expected", [
+    (dict(B=0), E_INVAL), (dict(H=0), E_INVAL), (dict(N=0), E_INVAL), (dict(N=-5), E_INVAL),
+    (dict(d=96), E_UNSUP), (dict(d=32), E_UNSUP), (dict(d=256), E_UNSUP),
+    (dict(scale=float("nan")), E_INVAL), (dict(scale=float("inf")), E_INVAL), (dict(scale=0.0), E_INVAL),
+    (dict(scale=-0.125), E_INVAL), (dict(B=65536, H=65536, N=2), E_INVAL),
+])
+def test_fwd_rejects_bad_sizes_and_scale(kw, expected):
+    b = Bufs()
+    assert fwd(b, **kw) == expected
+    assert b.untouched()
+
+
+@pytest.mark.parametrize("which", range(5))
+def test_fwd_rejects_null_and_misaligned_pointers(which):
+    b = Bufs()
+    assert fwd(b, override={which: None}) == E_INVAL
+    assert fwd(b, override={which: b.p(which) + 8}) == E_INVAL
+    assert b.untouched()
+
+
+def bwd(b, B=1, H=1, N=8, d=64, scale=0.125, ws_bytes=None, override=None):
+    ptrs = [b.p(i) for i in range(9)]
+    if override:
+        for i, val in override.items():
+            if i < 9:
+                ptrs[i] = val
+    ws = b.p(9)
+    if override and 9 in override:
+        ws = override[9]
+    wsb = va.workspace_bytes(max(B, 1), max(H, 1), max(N, 1), d if d in (64, 128) else 64) if ws_bytes is None \
+        else ws_bytes
+    return lib().vitattn_bwd(*ptrs, B, H, N, d, scale, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,expected", [
+    (dict(N=0), E_INVAL), (dict(d=80), E_UNSUP), (dict(scale=float("nan")), E_INVAL),
+    (dict(ws_bytes=31), E_WS), (dict(ws_bytes=0), E_WS), (dict(override={9: None}), E_WS),
+    (dict(override={9: 12345}), E_WS),
+])
+def test_bwd_rejects_bad_arguments(kw, expected):
+    b = Bufs()
+    assert bwd(b, **kw) == expected
+    assert b.untouched()
+
+
+@pytest.mark.parametrize("which", range(9))
+def test_bwd_rejects_null_pointers(which):
+    b = Bufs()
+    assert bwd(b, override={which: None}) == E_INVAL
+    assert bwd(b, override={which: b.p(which) + 4}) == E_INVAL
+    assert b.untouched()
+
+
+def test_bwd_stages_validate():
+    b = Bufs()
+    L = lib()
+    wsb = va.workspace_bytes(1, 1, 8, 64)
+    assert L.vitattn_bwd_rowdot(b.p(0), b.p(1), 1, 1, 8, 64, b.p(2), wsb - 1, None) == E_WS
+    assert L.vitattn_bwd_rowdot(None, b.p(1), 1, 1, 8, 64, b.p(2), wsb, None) == E_INVAL
+    assert L.vitattn_bwd_dkdv(b.p(0), b.p(1), b.p(2), b.p(3), b.p(4), b.p(5), b.p(6), 1, 1, 8, 100, 0.1, b.p(7), wsb,
+                              None) == E_UNSUP
+    assert L.vitattn_bwd_dkdv(b.p(0), b.p(1), b.p(2), b.p(3), None, b.p(5), b.p(6), 1, 1, 8, 64, 0.1, b.p(7), wsb,
+                              None) == E_INVAL
+    assert L.vitattn_bwd_dq(b.p(0), b.p(1), b.p(2), b.p(3), b.p(4), b.p(5), 1, 1, 8, 64, -1.0, b.p(7), wsb,
+                            None) == E_INVAL
+    assert L.vitattn_bwd_dq(b.p(0), b.p(1), b.p(2), b.p(3), b.p(4), b.p(5), 1, 1, 8, 64, 0.1, b.p(7), 0,
+                            None) == E_WS
+    assert b.untouched()
+
+
+def test_binding_helpers_reject_wrong_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
+    with pytest.raises(TypeError):
+        va.fwd(x, x, x)  # CPU tensors are refused before any library call
+
+
+def test_product_package_does_not_import_the_oracle():
+    pkg_dir = os.path.join(ROOT, "paper_2405_15780_amd")
+    for dirpath, _, files in os.walk(pkg_dir):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(from|import)\s+oracle\b", text, flags=re.M), f
+                assert "oracle/" not in text, f
