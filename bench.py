@@ -1,0 +1,197 @@
+"""Benchmark: exact non-causal attention forward + backward on one MI355X.
+
+One step = the whole hot path over one batch: vitattn_fwd, then the three
+backward stages (rowdot preprocess, dK/dV, dQ), on inputs already resident in
+HBM. The default workload is the paper-scale shard B=1, H=2, N=188,416
+(368 x 512 patches = 92 channels x 2,048), d=128, bf16 inputs with fp32
+accumulation and outputs.
+
+value = counted FLOPs / step time, FlashAttention convention: forward
+4 B H N^2 d, backward 10 B H N^2 d (P's recomputation is not counted).
+
+Prints one JSON line. `roofline` describes the kernel with the largest share
+of the step time, timed with HIP events on the stream it is launched on
+(PyTorch's current stream, which the binding passes to the library).
+`cpu_baseline` times the fp64 oracle on a bounded slice of the same workload
+(a block of query rows of head 0, forward plus that block's backward work).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA (256 CU x 4096 flop/clk x 2.4 GHz)
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--config", type=int, default=4, help="workload id (4 = B1 H2 N188416 d128)")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+def cpu_baseline(w, x, budget_s):
+    import numpy as np
+
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # threadpoolctl missing: report the BLAS default
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    rows_per_block = 512
+    done = 0
+    t0 = time.perf_counter()
+    while done < w.N and time.perf_counter() - t0 < budget_s:
+        r1 = min(w.N, done + rows_per_block)
+        oracle.forward_backward_rows(x["q"], x["k"], x["v"], x["dout"], w.scale, 0, 0, done, r1)
+        done = r1
+    dt = time.perf_counter() - t0
+    flops = 14.0 * done * w.N * w.d if w.backward else 4.0 * done * w.N * w.d
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"fp64 forward+backward of query rows 0..{done - 1} of head 0 against all {w.N} keys "
+                  f"({done}/{w.B * w.H * w.N} of the workload's rows), {dt:.1f} s",
+        "seconds": dt,
+        "host_cpus": len(os.sched_getaffinity(0)),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2405_15780_amd as va
+    import workloads
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = workloads.CONFIGS[args.config]
+    B, H, N, d = w.shape
+    x = workloads.make_inputs(w, with_dout=True)
+    dev = torch.device("cuda:0")
+    t = {n: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev) for n, a in x.items()}
+    f32 = dict(dtype=torch.float32, device=dev)
+    o = torch.empty((B, H, N, d), **f32)
+    lse = torch.empty((B, H, N), **f32)
+    dq, dk, dv = (torch.empty((B, H, N, d), **f32) for _ in range(3))
+    ws = torch.empty(va.workspace_bytes(B, H, N, d) // 4, **f32)
+    scale = w.scale
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        va.fwd(t["q"], t["k"], t["v"], scale, out=(o, lse))
+        if w.backward:
+            if ev is not None:
+                ev[1].record()
+            va.bwd_rowdot(o, t["dout"], lse, ws)
+            if ev is not None:
+                ev[2].record()
+            va.bwd_dkdv(t["q"], t["k"], t["v"], t["dout"], lse, dk, dv, ws, scale)
+            if ev is not None:
+                ev[3].record()
+            va.bwd_dq(t["q"], t["k"], t["v"], t["dout"], lse, dq, ws, scale)
+        if ev is not None:
+            ev[4].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        step(events[i])
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / args.steps
+
+    names = ["fwd", "rowdot", "dkdv", "dq"] if w.backward else ["fwd"]
+    spans = {"fwd": (0, 1 if w.backward else 4), "rowdot": (1, 2), "dkdv": (2, 3), "dq": (3, 4)}
+    kern_ms = {n: float(np.mean([e[spans[n][0]].elapsed_time(e[spans[n][1]]) for e in events])) for n in names}
+
+    flops = w.counted_flops()
+    value = flops["total"] / (ms_per_step * 1e-3) / 1e12
+    nn = float(B * H) * N * N * d
+    # algorithmic work of one launch of each kernel
+    kern_work = {
+        "fwd": ("mfma", 4.0 * nn),                       # S = QK^T and O = PV
+        "dkdv": ("mfma", 8.0 * nn),                      # S, dP recomputed; dV += P^T dO; dK += dS^T Q
+        "dq": ("mfma", 6.0 * nn),                        # S, dP recomputed; dQ += dS K
+        "rowdot": ("hbm", float(B * H * N) * (2 * d + 4 * d + 12)),  # read dO bf16, O fp32, LSE; write D, LSE2
+    }
+    dom = max(names, key=lambda n: kern_ms[n])
+    bound, work = kern_work[dom]
+    if bound == "mfma":
+        achieved = work / (kern_ms[dom] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None, "kernel": dom}
+    else:
+        achieved = work / (kern_ms[dom] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": dom}
+
+    per_kernel = {}
+    for n in names:
+        b_, wk = kern_work[n]
+        per_kernel[n] = {"ms": kern_ms[n]}
+        if b_ == "mfma":
+            per_kernel[n]["tflops"] = wk / (kern_ms[n] * 1e-3) / 1e12
+            per_kernel[n]["frac_of_peak"] = per_kernel[n]["tflops"] / PEAK_BF16_TFLOPS
+        else:
+            per_kernel[n]["gbs"] = wk / (kern_ms[n] * 1e-3) / 1e9
+
+    result = {
+        "metric": "attention fwd+bwd TFLOP/s and % of bf16 MFMA peak at N=188,416, d=128",
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "H": H, "N": N, "d": d, "passes": "fwd+bwd" if w.backward else "fwd",
+                   "grid": f"{w.grid[0]}x{w.grid[1]}", "seed": w.seed},
+        "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
+        "counted_tflop_per_step": flops["total"] / 1e12,
+        "kernels": per_kernel,
+        "wall_s_timed": wall,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        print(f"# timing the oracle for ~{args.cpu_seconds:.0f} s", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, x, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

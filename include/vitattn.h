@@ -25,7 +25,9 @@
  *    backward workspace are [B][H][N]. Element offsets use 64-bit arithmetic.
  *  - q, k, v and dout hold bfloat16 values as raw 16-bit patterns. o, lse, dq,
  *    dk and dv are fp32. Every pointer must be 16-byte aligned.
- *  - Supported head dims: d = 64 and d = 128. Any N >= 1.
+ *  - Supported head dims: d = 64 and d = 128. Any N >= 1 with (N + 256)*d*2
+ *    below 2^31 (the kernels address one head's rows with 32-bit offsets;
+ *    N up to 8,388,351 at d = 128) and B*H*N below 2^31.
  *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *    the call returns without waiting. Execution faults surface at the
  *    caller's next synchronisation on that stream.
@@ -67,8 +69,9 @@ int vitattn_fwd(const void* q, const void* k, const void* v, float* o, float* ls
                 float scale, void* stream);
 
 /*
- * Bytes of device workspace vitattn_bwd needs: 4*B*H*N (the fp32 row
- * statistic D) rounded up to 256. Returns 0 for invalid sizes.
+ * Bytes of device workspace vitattn_bwd needs: two fp32 [B][H][N] regions,
+ * each padded to a multiple of 64 rows (256 bytes): the row statistic D and
+ * LSE * log2(e). Returns 0 for invalid sizes.
  */
 size_t vitattn_bwd_workspace_bytes(int B, int H, int N, int d);
 
@@ -93,13 +96,13 @@ int vitattn_bwd(const void* q, const void* k, const void* v, const float* o, con
  * The three stages of vitattn_bwd, callable one by one (same arguments,
  * layouts and validation as vitattn_bwd; used to time each kernel). They
  * must run in this order on one stream, all with the same workspace:
- *   vitattn_bwd_rowdot: workspace <- D_i = sum_c dout_ic o_ic  (fp32 [B][H][N]);
+ *   vitattn_bwd_rowdot: workspace <- D_i = sum_c dout_ic o_ic and LSE_i*log2(e);
  *   vitattn_bwd_dkdv  : dk, dv from q, k, v, dout, lse and D in the workspace;
  *   vitattn_bwd_dq    : dq from q, k, v, dout, lse and D in the workspace.
  * Each stage validates its own arguments like vitattn_bwd does.
  */
-int vitattn_bwd_rowdot(const float* o, const void* dout, int B, int H, int N, int d, void* workspace,
-                       size_t workspace_bytes, void* stream);
+int vitattn_bwd_rowdot(const float* o, const void* dout, const float* lse, int B, int H, int N, int d,
+                       void* workspace, size_t workspace_bytes, void* stream);
 int vitattn_bwd_dkdv(const void* q, const void* k, const void* v, const void* dout, const float* lse, float* dk,
                      float* dv, int B, int H, int N, int d, float scale, const void* workspace,
                      size_t workspace_bytes, void* stream);

@@ -17,6 +17,7 @@ from .attention import (  # noqa: F401
     fp32_scale,
     forward,
     forward_backward,
+    forward_backward_rows,
     query_rows,
     row_statistics,
     key_rows,

@@ -123,6 +123,16 @@ def forward_backward(q, k, v, dout, scale, block=QUERY_BLOCK, heads=None):
     return out
 
 
+def forward_backward_rows(q, k, v, dout, scale, b, h, r0, r1):
+    """The forward and backward work of query rows r0..r1-1 of head (b, h)
+    against all keys: their o, lse, D and dq, plus their contributions
+    dk_part and dv_part to dK and dV (summing these over all row ranges gives
+    dK and dV). Used to time the oracle on a bounded slice of a workload."""
+    s = fp32_scale(scale)
+    return _block_backward(_as_f64(q[b, h, r0:r1]), _as_f64(k[b, h]), _as_f64(v[b, h]), _as_f64(dout[b, h, r0:r1]),
+                           s)
+
+
 def query_rows(q, k, v, scale, rows, dout=None):
     """Per-row outputs for sampled query rows.
 

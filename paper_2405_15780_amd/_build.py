@@ -20,6 +20,9 @@ HIP_FLAGS = [
     "-Wall",
     # packed fp32 VALU forms stay disabled on this target
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep matrix-core accumulators in VGPR form: otherwise the allocator
+    # parks loop-carried accumulators in AGPRs and copies them every trip
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
 ]
 
 

@@ -23,7 +23,7 @@ _SIGNATURES = {
     "vitattn_fwd": (c_int, [c_void_p] * 5 + [c_int] * 4 + [c_float, c_void_p]),
     "vitattn_bwd_workspace_bytes": (c_size_t, [c_int] * 4),
     "vitattn_bwd": (c_int, [c_void_p] * 9 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
-    "vitattn_bwd_rowdot": (c_int, [c_void_p] * 2 + [c_int] * 4 + [c_void_p, c_size_t, c_void_p]),
+    "vitattn_bwd_rowdot": (c_int, [c_void_p] * 3 + [c_int] * 4 + [c_void_p, c_size_t, c_void_p]),
     "vitattn_bwd_dkdv": (c_int, [c_void_p] * 7 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
     "vitattn_bwd_dq": (c_int, [c_void_p] * 6 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
     "vitattn_status_str": (ctypes.c_char_p, [c_int]),
@@ -136,9 +136,9 @@ def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None):
     return dq, dk, dv
 
 
-def bwd_rowdot(o, dout, workspace):
+def bwd_rowdot(o, dout, lse, workspace):
     B, H, N, d = dout.shape
-    _check(library().vitattn_bwd_rowdot(o.data_ptr(), dout.data_ptr(), B, H, N, d, workspace.data_ptr(),
+    _check(library().vitattn_bwd_rowdot(o.data_ptr(), dout.data_ptr(), lse.data_ptr(), B, H, N, d, workspace.data_ptr(),
                                         workspace.numel() * workspace.element_size(), _stream_ptr(dout)))
 
 

@@ -3,6 +3,7 @@
 // launched nothing and written nothing, and works without a GPU.
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include <exception>
 
@@ -21,12 +22,21 @@ int check_sizes(int B, int H, int N, int d) {
   // row indices and grid sizes are 32-bit: B*H*N must fit in an int
   const long long rows = (long long)B * H * N;
   if (rows > 0x7fffffffLL) return VITATTN_E_INVAL;
+  // per-head byte offsets (plus one tile of padding) must fit in 31 bits
+  if ((long long)(N + 256) * d * 2 > 0x7fffffffLL) return VITATTN_E_INVAL;
   return VITATTN_OK;
 }
 
 bool scale_ok(float s) { return isfinite(s) && s > 0.f; }
 
 }  // namespace
+
+namespace vitattn {
+int tuning_variant(const char* env_name) {
+  const char* s = getenv(env_name);
+  return s ? atoi(s) : 0;
+}
+}  // namespace vitattn
 
 extern "C" {
 
@@ -46,8 +56,7 @@ const char* vitattn_version(void) { return VITATTN_VERSION; }
 
 size_t vitattn_bwd_workspace_bytes(int B, int H, int N, int d) {
   if (check_sizes(B, H, N, d) != VITATTN_OK) return 0;
-  const size_t bytes = (size_t)B * H * N * sizeof(float);
-  return (bytes + 255) & ~(size_t)255;
+  return 2 * vitattn::bwd_region_floats((long long)B * H * N) * sizeof(float);
 }
 
 int vitattn_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int N, int d,
@@ -96,6 +105,7 @@ static vitattn::BwdArgs bwd_args(const void* q, const void* k, const void* v, co
   a.dk = dk;
   a.dv = dv;
   a.drow = static_cast<float*>(const_cast<void*>(workspace));
+  a.lse2 = a.drow + vitattn::bwd_region_floats((long long)B * H * N);
   a.BH = B * H;
   a.N = N;
   a.d = d;
@@ -123,16 +133,16 @@ int vitattn_bwd(const void* q, const void* k, const void* v, const float* o, con
   }
 }
 
-int vitattn_bwd_rowdot(const float* o, const void* dout, int B, int H, int N, int d, void* workspace,
-                       size_t workspace_bytes, void* stream) {
+int vitattn_bwd_rowdot(const float* o, const void* dout, const float* lse, int B, int H, int N, int d,
+                       void* workspace, size_t workspace_bytes, void* stream) {
   try {
     int st = check_sizes(B, H, N, d);
     if (st != VITATTN_OK) return st;
-    if (!aligned16(o) || !aligned16(dout)) return VITATTN_E_INVAL;
+    if (!aligned16(o) || !aligned16(dout) || !aligned16(lse)) return VITATTN_E_INVAL;
     st = check_workspace(workspace, workspace_bytes, B, H, N, d);
     if (st != VITATTN_OK) return st;
-    const vitattn::BwdArgs a = bwd_args(nullptr, nullptr, nullptr, o, dout, nullptr, nullptr, nullptr, nullptr, B, H,
-                                        N, d, 1.f, workspace, stream);
+    const vitattn::BwdArgs a = bwd_args(nullptr, nullptr, nullptr, o, dout, lse, nullptr, nullptr, nullptr, B, H, N,
+                                        d, 1.f, workspace, stream);
     return vitattn::launch_bwd_rowdot(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
   } catch (...) {
     return VITATTN_E_INTERNAL;

@@ -12,6 +12,8 @@
 //        S^T = K Q^T, P^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T
 // Splitting dQ from dK/dV costs one extra recomputation of S and dP but needs
 // no atomics, so results are deterministic.
+#include <type_traits>
+
 #include "vitattn_common.h"
 #include "vitattn_launch.h"
 
@@ -22,10 +24,14 @@ constexpr int kBwdThreads = 64 * kBwdWaves;
 
 // ------------------------------------------------------------------ preprocess
 
+// Writes the two per-row statistics the backward kernels stream: D_i =
+// sum_c dO_ic O_ic and LSE_i * log2(e) (the logsumexp in the base-2 units of
+// the kernels' exp2). Each lives in its own region of the workspace.
 template <int D>
 __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __restrict__ dout,
-                                                              const float* __restrict__ o, float* __restrict__ drow,
-                                                              long rows) {
+                                                              const float* __restrict__ o,
+                                                              const float* __restrict__ lse, float* __restrict__ drow,
+                                                              float* __restrict__ lse2, long rows) {
   constexpr int LPR = D / 8;  // lanes per row, 8 elements each
   const long row = (long)blockIdx.x * (256 / LPR) + threadIdx.x / LPR;
   const int part = threadIdx.x % LPR;
@@ -40,7 +46,10 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __
   }
 #pragma unroll
   for (int m = LPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
-  if (row < rows && part == 0) drow[row] = acc;
+  if (row < rows && part == 0) {
+    drow[row] = acc;
+    lse2[row] = lse[row] * kLog2e;
+  }
 }
 
 // ------------------------------------------------------------------ dK / dV
@@ -48,161 +57,197 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __
 constexpr int kDkvBK = 32 * kBwdWaves;  // keys per workgroup
 constexpr int kDkvBQ = 64;              // queries per streamed tile
 
-// Per-row statistics of a query tile (LSE in log2 units, and D), staged
-// through registers like the bf16 tiles. Rows at or past N get LSE = +inf
-// (so P = 0) and D = 0.
-struct RowStatLoader {
-  float val;
-  __device__ __forceinline__ void load(const float* __restrict__ lse, const float* __restrict__ drow, int row0,
-                                       int N, int tid) {
-    if (tid < kDkvBQ) {
-      const int row = row0 + tid;
-      val = row < N ? lse[row] * kLog2e : INFINITY;
-    } else if (tid < 2 * kDkvBQ) {
-      const int row = row0 + tid - kDkvBQ;
-      val = row < N ? drow[row] : 0.f;
-    }
-  }
-  __device__ __forceinline__ void store(float* s, int tid) const {
-    if (tid < 2 * kDkvBQ) s[tid] = val;
-  }
-};
+// Direct global -> LDS copy of a tile's row statistics: 64 floats of D and
+// 64 of LSE*log2(e) (one dword per lane; rows past the end read as zeros).
+// Every wave copies the same data, so that all waves issue the same number
+// of loads per tile and one vmcnt bound fits them all.
+__device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float* lds_stats, int lane) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, (lds_void_t*)(lds_stats), 4, (row0 + lane) * 4, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_void_t*)(lds_stats + kDkvBQ), 4, (row0 + lane) * 4, 0, 0, 0);
+}
 
+// One workgroup = 8 waves = 128 keys of one (b, h), in four blocks of 32
+// keys. Each key block has two waves with split roles (waves w and w+4 share
+// a SIMD, so their vector and matrix phases interleave):
+//   role P  (waves 0-3): holds K, accumulates dV^T.
+//     S = Q K^T;  P = exp2(S*scale*log2e - LSE2);  dV^T += dO^T P;
+//     writes P (bf16) to LDS for its partner.
+//   role dS (waves 4-7): holds V, accumulates dK^T, one tile behind.
+//     dP = dO V^T;  dS = P o (dP - D) with the partner's P;  dK^T += Q^T dS.
+// Q, dO and the row statistics stream through a ring of three LDS slots in
+// tiles of 64 queries (two blocks of 32); in iteration t role P works on
+// tile t and role dS on tile t-1, and tile t+1 is being fetched. Query rows
+// past the end arrive as zeros and then contribute exactly nothing (P =
+// exp2(0) = 1 multiplies dO = 0, and dS = P (dP - D) = 0).
+//
+// Each wave's work per tile is one stream of 4*D/16 matrix-core ops whose
+// LDS operands are read two ops ahead, in four phases (query blocks 0, 1):
+//   1. first product of block 0 (S or dP)
+//   2. first product of block 1;  vector units: P or dS of block 0
+//   3. second product of block 0 (dV or dK);  vector units: block 1
+//   4. second product of block 1
 template <int D>
-__global__ __launch_bounds__(kBwdThreads, 1) void attn_bwd_dkdv_kernel(
+__global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const uint16_t* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ drow,
+    const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
     float* __restrict__ dk, float* __restrict__ dv, int N, int n_ktiles, int total, float c, float scale) {
+  constexpr int KK = D / 16, NCB = D / 32;
+  constexpr int PH = KK;           // ops per phase
+  constexpr int NOPS = 4 * PH;     // ops per tile
+  constexpr int RPS = 16 / PH;     // query rows of vector work per op slot
   constexpr int TILE_BYTES = kDkvBQ * D * 2;
-  __shared__ __attribute__((aligned(16))) char smem[2][2][TILE_BYTES];  // [buffer][Q, dO]
-  __shared__ __attribute__((aligned(16))) float sstat[2][2 * kDkvBQ];    // [buffer][LSE2 | D]
+  constexpr int RING = 3;
+  constexpr int NWAVES = 2 * kBwdWaves;
+  __shared__ __attribute__((aligned(1024))) char qbuf[RING][TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char gbuf[RING][TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) float sbuf[RING][2 * kDkvBQ];  // [D | LSE2]
+  // P exchange: [buffer][key block][query block][contraction step][lane] of 8 bf16
+  __shared__ __attribute__((aligned(16))) uint4 xbuf[2][kBwdWaves][2][2][64];
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_ktiles;
   const int kt = work - bh * n_ktiles;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
+  const int kb = wave & 3;
+  const bool role_p = wave < 4;
 
   const size_t head_off = (size_t)bh * N * D;
-  const uint16_t* Q = q + head_off;
-  const uint16_t* dO = dout + head_off;
-  const float* L = lse + (size_t)bh * N;
-  const float* Dr = drow + (size_t)bh * N;
+  const unsigned head_bytes = (unsigned)N * (2 * D);
+  const rsrc_t rq = make_rsrc(q + head_off, head_bytes);
+  const rsrc_t rg = make_rsrc(dout + head_off, head_bytes);
+  const rsrc_t rd = make_rsrc(drow + (size_t)bh * N, (unsigned)N * 4);
+  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * N, (unsigned)N * 4);
 
-  // this wave's 32 keys: K and V fragments as B operands (columns = keys)
-  const int key = kt * kDkvBK + wave * 32 + (lane & 31);
-  bf16x8 kf[D / 16], vf[D / 16];
+  // held fragments (B operands, columns = this block's keys): K for role P, V for role dS
+  const int key = kt * kDkvBK + kb * 32 + (lane & 31);
+  const rsrc_t rh = make_rsrc((role_p ? k : v) + head_off, head_bytes);
+  bf16x8 hf[KK];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-    if (key < N) {
-      a = *reinterpret_cast<const uint4*>(k + head_off + (size_t)key * D + 16 * kk + 8 * h);
-      b = *reinterpret_cast<const uint4*>(v + head_off + (size_t)key * D + 16 * kk + 8 * h);
-    }
-    kf[kk] = as_bf16x8(a);
-    vf[kk] = as_bf16x8(b);
-  }
+  for (int kk = 0; kk < KK; ++kk) hf[kk] = as_bf16x8(buffer_load16(rh, key * (2 * D) + 32 * kk + 16 * h));
 
+  TileDma<D, kDkvBQ, NWAVES> dma;
+  dma.init(wave, lane);
   RowFrag<D> rf;
   rf.init(lane);
   TrFrag<D> tf;
   tf.init(lane);
+  constexpr int DMA_PER_TILE = 2 * decltype(dma)::PER_WAVE + 2;  // loads per wave per tile
 
-  f32x16 dkacc[D / 32], dvacc[D / 32];
+  f32x16 acc[NCB];  // dV^T (role P) or dK^T (role dS)
 #pragma unroll
-  for (int cb = 0; cb < D / 32; ++cb) {
-    dkacc[cb] = zero16();
-    dvacc[cb] = zero16();
-  }
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero16();
+
+  auto issue_tile = [&](int t) {
+    const int slot = t % RING;
+    dma.issue(rq, t * kDkvBQ, qbuf[slot]);
+    dma.issue(rg, t * kDkvBQ, gbuf[slot]);
+    stats_dma(rd, rl, t * kDkvBQ, sbuf[slot], lane);
+  };
+
+  // One tile of one role. ROLE_P: S/P/dV on tile t; otherwise dP/dS/dK.
+  auto run_tile = [&](auto role_tag, int t) {
+    constexpr bool RP = decltype(role_tag)::value;
+    const int slot = t % RING;
+    const char* qs = qbuf[slot];
+    const char* gs = gbuf[slot];
+    const float* st = sbuf[slot];
+    uint4(*xb)[2][64] = xbuf[t & 1][kb];
+
+    f32x16 m1[2];          // S (P) or dP (dS), per query block
+    bf16x8 ob[2][2];       // bf16 operands of P or dS [block][contraction step]
+    float4 stat[2][4];     // LSE2 (role P) or D (role dS) of the block's rows
+    uint4 pin4[2][2];      // role dS: the partner's P, as bf16 pairs
+
+    // A operand of op i
+    auto read_a = [&](int i) -> bf16x8 {
+      const int ph = i / PH, j = i % PH, qb = ph & 1;
+      if (ph < 2) return lds_frag_row(RP ? qs : gs, qb * 32 * 2 * D + rf.off[j]);
+      return tf.load(RP ? gs : qs, qb * 32 + 16 * (j / NCB), j % NCB);
+    };
+    auto read_side = [&](int qb) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        stat[qb][g] = *reinterpret_cast<const float4*>(st + (RP ? kDkvBQ : 0) + qb * 32 + 8 * g + 4 * h);
+      if constexpr (!RP) {
+        pin4[qb][0] = xb[qb][0][lane];
+        pin4[qb][1] = xb[qb][1][lane];
+      }
+    };
+    auto valu = [&](int qb, int u) {
+#pragma unroll
+      for (int rr = 0; rr < RPS; ++rr) {
+        const int r = u * RPS + rr;
+        const float sv = stat[qb][r >> 2][r & 3];
+        float x;
+        if constexpr (RP) {
+          x = __builtin_amdgcn_exp2f(__builtin_fmaf(m1[qb][r], c, -sv));
+        } else {
+          const unsigned w = pin4[qb][r >> 3][(r & 7) >> 1];
+          const float p = __uint_as_float((r & 1) ? (w & 0xffff0000u) : (w << 16));
+          x = p * (m1[qb][r] - sv);
+        }
+        pin(x);
+        m1[qb][r] = x;
+        if ((r & 7) == 7) ob[qb][r >> 3] = acc_to_operand(m1[qb], r >> 3);
+      }
+    };
+
+    bf16x8 aq[3];
+    aq[0] = read_a(0);
+    aq[1] = read_a(1);
+    read_side(0);
+    sched_fence();
+#pragma unroll
+    for (int i = 0; i < NOPS; ++i) {
+      if (i + 2 < NOPS) aq[(i + 2) % 3] = read_a(i + 2);
+      const int ph = i / PH, j = i % PH, qb = ph & 1;
+      if (ph < 2) {
+        if (j == 0) m1[qb] = zero16();
+        m1[qb] = mfma32(aq[i % 3], hf[j], m1[qb]);
+        if (ph == 1) {
+          if (j == 0) read_side(1);
+          valu(0, j);
+        }
+      } else {
+        acc[j % NCB] = mfma32(aq[i % 3], ob[qb][j / NCB], acc[j % NCB]);
+        if (ph == 2) valu(1, j);
+      }
+      sched_fence();
+    }
+    if constexpr (RP) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) xb[qb][ks][lane] = __builtin_bit_cast(uint4, ob[qb][ks]);
+    }
+  };
 
   const int n_qt = (N + kDkvBQ - 1) / kDkvBQ;
-  TileLoader<D, kDkvBQ, kBwdThreads> ql, gl;
-  RowStatLoader sl;
-  ql.load(Q, 0, N, tid);
-  gl.load(dO, 0, N, tid);
-  sl.load(L, Dr, 0, N, tid);
-  ql.store(smem[0][0], tid);
-  gl.store(smem[0][1], tid);
-  sl.store(sstat[0], tid);
+  issue_tile(0);
+  wait_vmem();
   __syncthreads();
-
-  for (int t = 0; t < n_qt; ++t) {
-    const int buf = t & 1;
-    const bool more = t + 1 < n_qt;
-    if (more) {
-      ql.load(Q, (t + 1) * kDkvBQ, N, tid);
-      gl.load(dO, (t + 1) * kDkvBQ, N, tid);
-      sl.load(L, Dr, (t + 1) * kDkvBQ, N, tid);
+  for (int t = 0; t <= n_qt; ++t) {
+    if (t + 1 < n_qt) issue_tile(t + 1);
+    if (role_p) {
+      if (t < n_qt) run_tile(std::true_type{}, t);
+    } else {
+      if (t >= 1) run_tile(std::false_type{}, t - 1);
     }
-    const char* qs = smem[buf][0];
-    const char* gs = smem[buf][1];
-    const float* st = sstat[buf];
-
-#pragma unroll
-    for (int qb = 0; qb < kDkvBQ / 32; ++qb) {
-      // S = Q K^T (rows = queries, columns = this wave's keys)
-      f32x16 s = zero16();
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) s = mfma32(lds_frag_row(qs, qb * 32 * 2 * D + rf.off[kk]), kf[kk], s);
-      // P = exp2(S c - LSE2[row])
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const float4 l4 = *reinterpret_cast<const float4*>(st + qb * 32 + 8 * g + 4 * h);
-        s[4 * g + 0] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[4 * g + 0], c, -l4.x));
-        s[4 * g + 1] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[4 * g + 1], c, -l4.y));
-        s[4 * g + 2] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[4 * g + 2], c, -l4.z));
-        s[4 * g + 3] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[4 * g + 3], c, -l4.w));
-      }
-      // dV^T += dO^T P
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const bf16x8 pf = acc_to_operand(s, ks);
-#pragma unroll
-        for (int cb = 0; cb < D / 32; ++cb) dvacc[cb] = mfma32(tf.load(gs, qb * 32 + 16 * ks, cb), pf, dvacc[cb]);
-      }
-      // dP = dO V^T
-      f32x16 dp = zero16();
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) dp = mfma32(lds_frag_row(gs, qb * 32 * 2 * D + rf.off[kk]), vf[kk], dp);
-      // dS = P o (dP - D[row])
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const float4 d4 = *reinterpret_cast<const float4*>(st + kDkvBQ + qb * 32 + 8 * g + 4 * h);
-        dp[4 * g + 0] = s[4 * g + 0] * (dp[4 * g + 0] - d4.x);
-        dp[4 * g + 1] = s[4 * g + 1] * (dp[4 * g + 1] - d4.y);
-        dp[4 * g + 2] = s[4 * g + 2] * (dp[4 * g + 2] - d4.z);
-        dp[4 * g + 3] = s[4 * g + 3] * (dp[4 * g + 3] - d4.w);
-      }
-      // dK^T += Q^T dS
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const bf16x8 df = acc_to_operand(dp, ks);
-#pragma unroll
-        for (int cb = 0; cb < D / 32; ++cb) dkacc[cb] = mfma32(tf.load(qs, qb * 32 + 16 * ks, cb), df, dkacc[cb]);
-      }
-    }
-    if (more) {
-      ql.store(smem[buf ^ 1][0], tid);
-      gl.store(smem[buf ^ 1][1], tid);
-      sl.store(sstat[buf ^ 1], tid);
-    }
+    wait_vmem();
     __syncthreads();
   }
+  (void)DMA_PER_TILE;
 
   if (key < N) {
-    float* dkrow = dk + head_off + (size_t)key * D;
-    float* dvrow = dv + head_off + (size_t)key * D;
+    float* out = (role_p ? dv : dk) + head_off + (size_t)key * D;
+    const float f = role_p ? 1.f : scale;
 #pragma unroll
-    for (int cb = 0; cb < D / 32; ++cb)
+    for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int col = 32 * cb + 8 * g + 4 * h;
-        *reinterpret_cast<float4*>(dkrow + col) =
-            make_float4(dkacc[cb][4 * g] * scale, dkacc[cb][4 * g + 1] * scale, dkacc[cb][4 * g + 2] * scale,
-                        dkacc[cb][4 * g + 3] * scale);
-        *reinterpret_cast<float4*>(dvrow + col) =
-            make_float4(dvacc[cb][4 * g], dvacc[cb][4 * g + 1], dvacc[cb][4 * g + 2], dvacc[cb][4 * g + 3]);
-      }
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<float4*>(out + 32 * cb + 8 * g + 4 * h) =
+            make_float4(acc[cb][4 * g] * f, acc[cb][4 * g + 1] * f, acc[cb][4 * g + 2] * f, acc[cb][4 * g + 3] * f);
   }
 }
 
@@ -326,7 +371,7 @@ static hipError_t rowdot_d(const BwdArgs& a) {
   const long rows = (long)a.BH * a.N;
   constexpr int rows_per_block = 256 / (D / 8);
   hipLaunchKernelGGL(attn_bwd_rowdot_kernel<D>, dim3((unsigned)((rows + rows_per_block - 1) / rows_per_block)),
-                     dim3(256), 0, a.stream, a.dout, a.o, a.drow, rows);
+                     dim3(256), 0, a.stream, a.dout, a.o, a.lse, a.drow, a.lse2, rows);
   return hipGetLastError();
 }
 
@@ -334,10 +379,19 @@ template <int D>
 static hipError_t dkdv_d(const BwdArgs& a) {
   const int n_kt = (a.N + kDkvBK - 1) / kDkvBK;
   const int total = a.BH * n_kt;
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<D>, dim3(total), dim3(kBwdThreads), 0, a.stream, a.q, a.k, a.v, a.dout,
-                     a.lse, a.drow, a.dk, a.dv, a.N, n_kt, total, a.scale * kLog2e, a.scale);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(total), dim3(2 * kBwdThreads), 0, a.stream, a.q, a.k, a.v,
+                     a.dout, a.drow, a.lse2, a.dk, a.dv, a.N, n_kt, total, a.scale * kLog2e, a.scale);
   return hipGetLastError();
 }
+
+#define VITATTN_DKDV_INSTANTIATE(D)                                                                         \
+  template __global__ void attn_bwd_dkdv_kernel<D>(                                                        \
+      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,            \
+      const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
+      float* __restrict__, int, int, int, float, float);
+VITATTN_DKDV_INSTANTIATE(128)
+VITATTN_DKDV_INSTANTIATE(64)
+#undef VITATTN_DKDV_INSTANTIATE
 
 template <int D>
 static hipError_t dq_d(const BwdArgs& a) {

@@ -163,6 +163,85 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
   return x * q + (x < rem ? x : rem) + j;
 }
 
+// Value of lane l^32 combined with lane l's own: v_permlane32_swap on (v, v)
+// yields v[l%32] and v[32 + l%32] in every lane.
+__device__ __forceinline__ float max_halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }
+
+// ------------------------------------------------------------ buffer loads
+// A raw buffer resource over `bytes` bytes from `base`: loads at offsets at
+// or past `bytes` return zeros without touching memory, which is how tile
+// loads handle the ragged end of a sequence without branches.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 buffer_load16(rsrc_t r, int byte_off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
+}
+
+// Direct global -> LDS copy of an R x D bf16 tile (rows row0 .. row0+R-1 of
+// a [N][D] matrix behind `r`) into the swizzled layout of tile_off. One
+// wave instruction fills 1 KB of consecutive LDS (16 bytes per lane), so
+// each lane fetches the chunk whose swizzled home is its LDS slot. Rows past
+// the end read as zeros. The NW waves of the group split the instructions.
+template <int D, int R, int NW>
+struct TileDma {
+  static constexpr int CH = D / 8;
+  static constexpr int INSTR = R * CH / 64;  // wave instructions per tile
+  static constexpr int PER_WAVE = INSTR >= NW ? INSTR / NW : 1;
+  static_assert(INSTR % NW == 0 || NW % INSTR == 0, "tile must divide evenly among waves");
+  int voff[PER_WAVE];  // byte offset of this lane's chunk relative to row0
+  int lds_off;         // LDS byte offset of this wave's first instruction
+  bool active;         // false for waves left without work on small tiles
+
+  __device__ __forceinline__ void init(int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int gi = (wave * PER_WAVE + i) % INSTR;
+      const int pos = gi * 64 + lane;  // 16-byte slot in the tile
+      const int row = pos / CH, pc = pos % CH;
+      voff[i] = row * (2 * D) + 16 * (pc ^ swz<D>(row));
+    }
+    lds_off = (wave * PER_WAVE) % INSTR * 1024;
+    active = wave * PER_WAVE < INSTR;
+  }
+  __device__ __forceinline__ void issue(rsrc_t r, int row0, char* lds_tile) const {
+    if (!active) return;
+    const int base = row0 * (2 * D);
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(lds_tile + lds_off + i * 1024), 16, base + voff[i], 0,
+                                               0, 0);
+  }
+};
+
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most CNT of this wave's vector memory loads are in flight
+// (loads complete in issue order for this count).
+template <int CNT>
+__device__ __forceinline__ void wait_vmem_leave() {
+  static_assert(CNT >= 0 && CNT < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CNT) : "memory");
+}
+
+// Full scheduling fence: nothing moves across it. Used to pin an explicit
+// software pipeline (each step: one matrix-core op, the LDS read of an
+// operand needed a few steps later, a slice of unrelated vector work);
+// left alone, the scheduler sinks every LDS read next to its consumer and
+// the wave then waits out the LDS latency before every op.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+// Force a value to be computed before this point (IR passes otherwise sink
+// pure arithmetic such as exp2 past the fences, towards its first use).
+__device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 
 }  // namespace vitattn

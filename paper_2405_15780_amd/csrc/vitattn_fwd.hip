@@ -1,37 +1,57 @@
 // Forward pass of exact non-causal attention for gfx950: tiled online softmax
 // (FlashAttention-2, cited by the paper in Sec. II-F) on bf16 matrix cores.
 //
-// One workgroup = 4 waves = 128 query rows of one (b, h); each wave owns 32
-// query rows. The workgroup streams K and V in tiles of 64 keys through a
-// double-buffered LDS ring; the next tile is fetched into registers with
-// 16-byte coalesced loads while the current one is being used.
+// One workgroup = NW waves = 32*NW query rows of one (b, h); each wave owns
+// 32 query rows and keeps their Q fragments in registers. K and V stream
+// through LDS in tiles of 32*KB keys, copied straight from HBM into the
+// swizzled LDS layout by buffer loads (rows past the end arrive as zeros).
 //
 // Per tile and wave:
 //   S^T (keys x queries) = K Q^T   -> each lane holds one query's scores
 //   running max / sum per query    -> in-lane, plus one exchange with lane^32
 //   P^T = exp2(S^T * scale*log2e - m)
 //   O^T (d x queries) += V^T P^T   -> P^T is reused in place as the operand
+//
+// Software pipeline across tiles: the scores of tile j+1 are computed on the
+// matrix cores while the vector units turn tile j's scores into
+// probabilities. K therefore runs one tile ahead of V, in two LDS rings of
+// RING slots: iteration j reads K_{j+1} and V_j and refills the slots of K_j
+// and V_{j-1} with K_{j+RING} and V_{j+RING-1}, so every tile is requested
+// RING-1 iterations before it is used (a tile that misses in L2 then does
+// not stall the workgroup at the next barrier).
+//
+// Software pipeline within a tile: each matrix-core op's LDS operand is read
+// two ops ahead, and the softmax is cut into slices placed between the score
+// ops, with scheduling fences pinning that order (the LDS read latency is
+// then hidden behind the ops instead of stalling each of them).
+//
 // The rescale of O by exp2(m_old - m_new) is skipped when no query of the
 // wave raised its running max (multiplying by 1 would change nothing), so
 // the maximum is always subtracted exactly and the largest P is exactly 1.
+#include <type_traits>
+
 #include "vitattn_common.h"
 #include "vitattn_launch.h"
 
 namespace vitattn {
 
-constexpr int kFwdWaves = 4;
-constexpr int kFwdThreads = 64 * kFwdWaves;
-constexpr int kFwdBM = 32 * kFwdWaves;  // query rows per workgroup
-constexpr int kFwdBN = 64;              // keys per tile
-
-template <int D>
-__global__ __launch_bounds__(kFwdThreads, 2) void attn_fwd_kernel(const uint16_t* __restrict__ q,
-                                                                   const uint16_t* __restrict__ k,
-                                                                   const uint16_t* __restrict__ v,
-                                                                   float* __restrict__ o, float* __restrict__ lse,
-                                                                   int N, int n_qtiles, int total, float c) {
-  constexpr int TILE_BYTES = kFwdBN * D * 2;
-  __shared__ __attribute__((aligned(16))) char smem[2][2][TILE_BYTES];  // [buffer][K, V]
+template <int D, int KB, int NW, int MINW, int RING>
+__global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t* __restrict__ q,
+                                                                 const uint16_t* __restrict__ k,
+                                                                 const uint16_t* __restrict__ v,
+                                                                 float* __restrict__ o, float* __restrict__ lse,
+                                                                 int N, int n_qtiles, int total, float c) {
+  constexpr int BM = 32 * NW;  // query rows per workgroup
+  constexpr int BN = 32 * KB;  // keys per tile
+  constexpr int TILE_BYTES = BN * D * 2;
+  constexpr int KK = D / 16;           // contraction steps of one 32-key score block
+  constexpr int NS = KB * KK;          // score ops per tile
+  constexpr int NV = 2 * KB * D / 32;  // PV ops per tile
+  constexpr int NSC = 16 * KB;         // scores per lane per tile
+  constexpr int LA = RING - 1;         // tiles requested ahead
+  static_assert(RING >= 2, "ring of at least two slots");
+  __shared__ __attribute__((aligned(1024))) char kbuf[RING][TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf[RING][TILE_BYTES];
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;
@@ -40,20 +60,19 @@ __global__ __launch_bounds__(kFwdThreads, 2) void attn_fwd_kernel(const uint16_t
   const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
 
   const size_t head_off = (size_t)bh * N * D;
-  const uint16_t* Q = q + head_off;
-  const uint16_t* K = k + head_off;
-  const uint16_t* V = v + head_off;
+  const unsigned head_bytes = (unsigned)N * (2 * D);
+  const rsrc_t rq = make_rsrc(q + head_off, head_bytes);
+  const rsrc_t rk = make_rsrc(k + head_off, head_bytes);
+  const rsrc_t rv = make_rsrc(v + head_off, head_bytes);
 
-  // Q fragments of this wave's 32 query rows (B operand of K Q^T).
-  const int qrow = qt * kFwdBM + wave * 32 + (lane & 31);
-  bf16x8 qf[D / 16];
+  // Q fragments of this wave's 32 query rows (B operands of K Q^T)
+  const int qrow = qt * BM + wave * 32 + (lane & 31);
+  bf16x8 qf[KK];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    uint4 u = make_uint4(0, 0, 0, 0);
-    if (qrow < N) u = *reinterpret_cast<const uint4*>(Q + (size_t)qrow * D + 16 * kk + 8 * h);
-    qf[kk] = as_bf16x8(u);
-  }
+  for (int kk = 0; kk < KK; ++kk) qf[kk] = as_bf16x8(buffer_load16(rq, qrow * (2 * D) + 32 * kk + 16 * h));
 
+  TileDma<D, BN, NW> dma;
+  dma.init(wave, lane);
   RowFrag<D> kfrag;
   kfrag.init(lane);
   TrFrag<D> vfrag;
@@ -65,86 +84,143 @@ __global__ __launch_bounds__(kFwdThreads, 2) void attn_fwd_kernel(const uint16_t
   float m_run = -INFINITY;  // running max of scaled logits, log2 units
   float l_part = 0.f;       // this lane's share of the row sum
 
-  const int n_ktiles = (N + kFwdBN - 1) / kFwdBN;
-  TileLoader<D, kFwdBN, kFwdThreads> kl, vl;
-  kl.load(K, 0, N, tid);
-  vl.load(V, 0, N, tid);
-  kl.store(smem[0][0], tid);
-  vl.store(smem[0][1], tid);
+  // operand reads of the score op i (K rows) and of the PV op i (V^T)
+  auto read_k = [&](const char* ks, int i) { return lds_frag_row(ks, (i / KK) * 32 * 2 * D + kfrag.off[i % KK]); };
+  auto read_v = [&](const char* vs, int i) { return vfrag.load(vs, (i / (D / 32)) * 16, i % (D / 32)); };
+
+  const int n_kt = (N + BN - 1) / BN;
+  // prologue: K_0 .. K_LA and V_0 .. V_{LA-1} (tiles past the end read as zeros)
+#pragma unroll
+  for (int t = 0; t < LA; ++t) {
+    dma.issue(rk, t * BN, kbuf[t]);
+    dma.issue(rv, t * BN, vbuf[t]);
+  }
+  dma.issue(rk, LA * BN, kbuf[LA]);
+  wait_vmem();
   __syncthreads();
+  f32x16 s[KB];
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    if (i % KK == 0) s[i / KK] = zero16();
+    s[i / KK] = mfma32(read_k(kbuf[0], i), qf[i % KK], s[i / KK]);
+  }
+  __syncthreads();  // kbuf[0] is refilled by the first iteration
 
-  for (int t = 0; t < n_ktiles; ++t) {
-    const int buf = t & 1;
-    const bool more = t + 1 < n_ktiles;
-    if (more) {
-      kl.load(K, (t + 1) * kFwdBN, N, tid);
-      vl.load(V, (t + 1) * kFwdBN, N, tid);
+  // One pipeline stage: softmax and PV of tile j, scores of tile j+1.
+  auto stage = [&](auto has_next, int j) {
+    constexpr bool NEXT = decltype(has_next)::value;
+    f32x16 sn[KB];
+    if constexpr (NEXT) {
+      dma.issue(rk, (j + 1 + LA) * BN, kbuf[(j + 1 + LA) % RING]);
+      dma.issue(rv, (j + LA) * BN, vbuf[(j + LA) % RING]);
+    } else {
+      // the last tile may be ragged: keys past the end get -inf
+      const int key0 = j * BN;
+      if (key0 + BN > N) {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (key0 + kb * 32 + acc_row(r, h) >= N) s[kb][r] = -INFINITY;
+      }
     }
-    const char* ks = smem[buf][0];
-    const char* vs = smem[buf][1];
+    const char* ks = kbuf[(j + 1) % RING];
+    const char* vs = vbuf[j % RING];
 
-    // S^T = K Q^T for two blocks of 32 keys
-    f32x16 s[2];
+    // softmax state, filled slice by slice
+    float mx0 = -INFINITY, mx1 = -INFINITY, m_new = 0.f, alpha = 1.f, lsum = 0.f;
+    bool raise = false;
+    // slices: 0 and 1 reduce half of the scores each; 2 finishes the max;
+    // the rest exponentiate an equal share of the scores
+    constexpr int NSLICE = NS > 3 ? NS : 4;
+    auto slice = [&](int i) {
+      if (i == 0) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      s[kb] = zero16();
+        for (int e = 0; e < NSC / 2; ++e) mx0 = fmaxf(mx0, s[e / 16][e % 16]);
+        pin(mx0);
+      } else if (i == 1) {
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
-        s[kb] = mfma32(lds_frag_row(ks, kb * 32 * 2 * D + kfrag.off[kk]), qf[kk], s[kb]);
+        for (int e = NSC / 2; e < NSC; ++e) mx1 = fmaxf(mx1, s[e / 16][e % 16]);
+        pin(mx1);
+      } else if (i == 2) {
+        const float m_tile = max_halves(fmaxf(mx0, mx1)) * c;
+        raise = m_tile > m_run;
+        m_new = fmaxf(m_run, m_tile);
+        alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        pin(m_new);
+      } else {
+        constexpr int NE = NSLICE - 3;
+        const int e0 = (i - 3) * NSC / NE, e1 = (i - 2) * NSC / NE;
+#pragma unroll
+        for (int e = 0; e < NSC; ++e)
+          if (e >= e0 && e < e1) {
+            float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e / 16][e % 16], c, -m_new));
+            pin(p);
+            s[e / 16][e % 16] = p;
+            lsum += p;
+          }
+      }
+    };
+
+    if constexpr (NEXT) {
+      // scores of tile j+1 on the matrix cores, softmax of tile j in the gaps
+      bf16x8 kq[3];
+      kq[0] = read_k(ks, 0);
+      kq[1] = read_k(ks, 1);
+      sched_fence();
+#pragma unroll
+      for (int i = 0; i < NS; ++i) {
+        if (i + 2 < NS) kq[(i + 2) % 3] = read_k(ks, i + 2);
+        if (i % KK == 0) sn[i / KK] = zero16();
+        sn[i / KK] = mfma32(kq[i % 3], qf[i % KK], sn[i / KK]);
+        slice(i);
+        sched_fence();
+      }
+#pragma unroll
+      for (int i = NS; i < NSLICE; ++i) slice(i);
+    } else {
+#pragma unroll
+      for (int i = 0; i < NSLICE; ++i) slice(i);
     }
-    // keys past the end of the sequence (last tile only)
-    const int key0 = t * kFwdBN;
-    if (key0 + kFwdBN > N) {
+    l_part = l_part * alpha + lsum;
+    bf16x8 pf[2 * KB];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (key0 + kb * 32 + acc_row(r, h) >= N) s[kb][r] = -INFINITY;
-    }
-    // running max per query (lanes l and l^32 share a query)
-    float mx = s[0][0];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, xor32(mx));
-    const float m_tile = mx * c;
-    if (__any(m_tile > m_run)) {
-      const float m_new = fmaxf(m_run, m_tile);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_part *= alpha;
+    for (int ks2 = 0; ks2 < 2 * KB; ++ks2) pf[ks2] = acc_to_operand(s[ks2 >> 1], ks2 & 1);
+    if (__any(raise)) {
 #pragma unroll
       for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
     }
-    // P^T = exp2(S^T c - m), row sums
+    // O^T += V^T P^T, V^T fragments read two ops ahead
+    {
+      bf16x8 vq[3];
+      vq[0] = read_v(vs, 0);
+      vq[1] = read_v(vs, 1);
+      sched_fence();
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][r], c, -m_run));
-        s[kb][r] = p;
-        l_part += p;
+      for (int i = 0; i < NV; ++i) {
+        if (i + 2 < NV) vq[(i + 2) % 3] = read_v(vs, i + 2);
+        const int cb = i % (D / 32);
+        oacc[cb] = mfma32(vq[i % 3], pf[i / (D / 32)], oacc[cb]);
+        sched_fence();
       }
-    // O^T += V^T P^T over 4 contraction steps of 16 keys
-#pragma unroll
-    for (int kstep = 0; kstep < 4; ++kstep) {
-      const bf16x8 pf = acc_to_operand(s[kstep >> 1], kstep & 1);
-#pragma unroll
-      for (int cb = 0; cb < D / 32; ++cb) oacc[cb] = mfma32(vfrag.load(vs, kstep * 16, cb), pf, oacc[cb]);
     }
-    if (more) {
-      kl.store(smem[buf ^ 1][0], tid);
-      vl.store(smem[buf ^ 1][1], tid);
+    if constexpr (NEXT) {
+      // K_{j+2} and V_{j+1} must have landed; later requests may be in flight
+      wait_vmem_leave<(LA - 1) * 2 * decltype(dma)::PER_WAVE>();
+      __syncthreads();
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) s[kb] = sn[kb];
     }
-    __syncthreads();
-  }
+  };
+
+  for (int j = 0; j < n_kt - 1; ++j) stage(std::true_type{}, j);
+  stage(std::false_type{}, n_kt - 1);
 
   // epilogue: O = O^T / l (stored transposed back to [query][d]), LSE in nats.
-  // Lanes l and l^32 hold the same query, so both take the same branch.
-  const float l = l_part + xor32(l_part);
+  const float l = sum_halves(l_part);
   if (qrow < N) {
     const float inv = 1.0f / l;
     float* orow = o + head_off + (size_t)qrow * D;
@@ -160,18 +236,51 @@ __global__ __launch_bounds__(kFwdThreads, 2) void attn_fwd_kernel(const uint16_t
   }
 }
 
-template <int D>
-static hipError_t launch_fwd_d(const FwdArgs& a) {
-  const int n_qtiles = (a.N + kFwdBM - 1) / kFwdBM;
+template <int D, int KB, int NW, int MINW, int RING>
+static hipError_t launch_fwd_v(const FwdArgs& a) {
+  constexpr int BM = 32 * NW;
+  const int n_qtiles = (a.N + BM - 1) / BM;
   const int total = a.BH * n_qtiles;
   const float c = a.scale * kLog2e;
-  hipLaunchKernelGGL(attn_fwd_kernel<D>, dim3(total), dim3(kFwdThreads), 0, a.stream, a.q, a.k, a.v, a.o, a.lse,
-                     a.N, n_qtiles, total, c);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, KB, NW, MINW, RING>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v,
+                     a.o, a.lse, a.N, n_qtiles, total, c);
   return hipGetLastError();
 }
 
+// Every tile variant is instantiated explicitly: hipcc otherwise omits the
+// host-side launch stub of some instantiations reached only through this
+// dispatch, and the library then fails to load.
+#define VITATTN_FWD_VARIANTS(X)                                                                         \
+  X(128, 2, 8, 2, 2) X(128, 2, 8, 2, 3) X(128, 2, 8, 2, 4) X(128, 1, 4, 2, 3) X(128, 1, 4, 2, 4)     \
+      X(128, 1, 8, 2, 4) X(64, 2, 8, 2, 2) X(64, 2, 8, 2, 3) X(64, 2, 8, 2, 4) X(64, 1, 4, 2, 3)     \
+          X(64, 1, 4, 2, 4) X(64, 1, 8, 2, 4)
+#define VITATTN_FWD_INSTANTIATE(D, KB, NW, MINW, RING)                                                 \
+  template __global__ void attn_fwd_kernel<D, KB, NW, MINW, RING>(const uint16_t* __restrict__,       \
+                                                                  const uint16_t* __restrict__,       \
+                                                                  const uint16_t* __restrict__,       \
+                                                                  float* __restrict__, float* __restrict__, int, \
+                                                                  int, int, float);
+VITATTN_FWD_VARIANTS(VITATTN_FWD_INSTANTIATE)
+#undef VITATTN_FWD_INSTANTIATE
+
+// Tile variants (key blocks per tile, waves per workgroup, waves per SIMD,
+// ring slots); 0 is the default.
+template <int D>
+static hipError_t launch_fwd_d(const FwdArgs& a, int variant) {
+  switch (variant) {
+    case 1: return launch_fwd_v<D, 2, 8, 2, 2>(a);
+    case 2: return launch_fwd_v<D, 2, 8, 2, 3>(a);
+    case 3: return launch_fwd_v<D, 2, 8, 2, 4>(a);
+    case 4: return launch_fwd_v<D, 1, 4, 2, 3>(a);
+    case 5: return launch_fwd_v<D, 1, 4, 2, 4>(a);
+    case 6: return launch_fwd_v<D, 1, 8, 2, 4>(a);
+    default: return launch_fwd_v<D, 2, 8, 2, 3>(a);
+  }
+}
+
 hipError_t launch_fwd(const FwdArgs& a) {
-  return a.d == 128 ? launch_fwd_d<128>(a) : launch_fwd_d<64>(a);
+  const int variant = tuning_variant("VITATTN_FWD_VARIANT");
+  return a.d == 128 ? launch_fwd_d<128>(a, variant) : launch_fwd_d<64>(a, variant);
 }
 
 }  // namespace vitattn

@@ -27,13 +27,22 @@ struct BwdArgs {
   float* dq;
   float* dk;
   float* dv;
-  float* drow;  // workspace: D = rowsum(dO o O), [BH][N]
+  float* drow;  // workspace region 0: D = rowsum(dO o O), [BH][N]
+  float* lse2;  // workspace region 1: LSE * log2(e), [BH][N]
   int BH, N, d;
   float scale;
   hipStream_t stream;
 };
 
 hipError_t launch_fwd(const FwdArgs& a);
+
+// Workspace layout of the backward pass: two fp32 regions of region_floats
+// each (D, then LSE*log2(e)), every region 256-byte aligned.
+inline size_t bwd_region_floats(long long rows) { return (size_t)((rows + 63) / 64) * 64; }
+
+// Kernel tile variant chosen by an environment variable (for tuning sweeps
+// only; 0 or unset selects the default variant).
+int tuning_variant(const char* env_name);
 // Backward stages; launch_bwd runs all three in order.
 hipError_t launch_bwd_rowdot(const BwdArgs& a);
 hipError_t launch_bwd_dkdv(const BwdArgs& a);

@@ -44,9 +44,11 @@ def test_status_strings_and_version():
 
 
 def test_workspace_bytes():
-    assert va.workspace_bytes(1, 2, 188416, 128) == 4 * 2 * 188416
-    assert va.workspace_bytes(1, 1, 1, 64) == 256
-    assert va.workspace_bytes(1, 1, 65, 64) == 512
+    assert va.workspace_bytes(1, 2, 188416, 128) == 2 * 4 * 2 * 188416
+    assert va.workspace_bytes(1, 1, 1, 64) == 512
+    assert va.workspace_bytes(1, 1, 65, 64) == 1024
+    assert va.workspace_bytes(1, 1, 8388351, 128) > 0
+    assert va.workspace_bytes(1, 1, 8388352, 128) == 0
     assert va.workspace_bytes(1, 1, 0, 64) == 0
     assert va.workspace_bytes(1, 1, 10, 96) == 0
 
@@ -135,8 +137,9 @@ def test_bwd_stages_validate():
     b = Bufs()
     L = lib()
     wsb = va.workspace_bytes(1, 1, 8, 64)
-    assert L.vitattn_bwd_rowdot(b.p(0), b.p(1), 1, 1, 8, 64, b.p(2), wsb - 1, None) == E_WS
-    assert L.vitattn_bwd_rowdot(None, b.p(1), 1, 1, 8, 64, b.p(2), wsb, None) == E_INVAL
+    assert L.vitattn_bwd_rowdot(b.p(0), b.p(1), b.p(3), 1, 1, 8, 64, b.p(2), wsb - 1, None) == E_WS
+    assert L.vitattn_bwd_rowdot(None, b.p(1), b.p(3), 1, 1, 8, 64, b.p(2), wsb, None) == E_INVAL
+    assert L.vitattn_bwd_rowdot(b.p(0), b.p(1), None, 1, 1, 8, 64, b.p(2), wsb, None) == E_INVAL
     assert L.vitattn_bwd_dkdv(b.p(0), b.p(1), b.p(2), b.p(3), b.p(4), b.p(5), b.p(6), 1, 1, 8, 100, 0.1, b.p(7), wsb,
                               None) == E_UNSUP
     assert L.vitattn_bwd_dkdv(b.p(0), b.p(1), b.p(2), b.p(3), None, b.p(5), b.p(6), 1, 1, 8, 64, 0.1, b.p(7), wsb,

@@ -220,6 +220,18 @@ def test_query_rows_and_key_rows_match_full_pass():
     np.testing.assert_allclose(dv, full["dv"][1, 0, keys], rtol=1e-11, atol=1e-13)
 
 
+def test_row_ranges_sum_to_full_pass():
+    rng = np.random.default_rng(15)
+    bits = {n: workloads.random_bf16(rng, (1, 2, 90, 8)) for n in ("q", "k", "v", "dout")}
+    full = oracle.forward_backward(bits["q"], bits["k"], bits["v"], bits["dout"], 0.375)
+    dk = np.zeros((90, 8))
+    for r0, r1 in ((0, 31), (31, 64), (64, 90)):
+        r = oracle.forward_backward_rows(bits["q"], bits["k"], bits["v"], bits["dout"], 0.375, 0, 1, r0, r1)
+        np.testing.assert_allclose(r["dq"], full["dq"][0, 1, r0:r1], rtol=1e-12, atol=1e-14)
+        dk += r["dk_part"]
+    np.testing.assert_allclose(dk, full["dk"][0, 1], rtol=1e-11, atol=1e-13)
+
+
 def test_bf16_decode_is_exact():
     bits = np.array([0x0000, 0x8000, 0x3F80, 0xBF80, 0x4049, 0x7F7F, 0x0001], dtype=np.uint16)
     expected = [0.0, -0.0, 1.0, -1.0, 3.140625, 3.3895313892515355e38, 9.183549615799121e-41]
