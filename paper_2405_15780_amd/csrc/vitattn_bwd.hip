@@ -253,16 +253,30 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 
 // ------------------------------------------------------------------ dQ
 
-constexpr int kDqBM = 32 * kBwdWaves;  // queries per workgroup
-constexpr int kDqBN = 64;              // keys per streamed tile
-
-template <int D>
-__global__ __launch_bounds__(kBwdThreads, 2) void attn_bwd_dq_kernel(
+// One workgroup = NW waves = 32*NW query rows of one (b, h); each wave owns
+// 32 queries and keeps their Q and dO fragments (B operands), their LSE2 and
+// D and the dQ^T accumulator in registers. K and V stream through a ring of
+// three LDS slots in tiles of 32 keys. Per tile j the wave runs
+//   S^T = K_{j+1} Q^T and dP^T = V_{j+1} dO^T   (matrix cores)
+//     interleaved with P^T, dS^T of tile j      (vector units)
+//   dQ^T += K_j^T dS^T_j
+// Key rows past the end arrive as zeros: their P is finite and they add
+// K_row^T dS = 0 to dQ, so no masking is needed.
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const uint16_t* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ drow,
+    const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
     float* __restrict__ dq, int N, int n_qtiles, int total, float c, float scale) {
-  constexpr int TILE_BYTES = kDqBN * D * 2;
-  __shared__ __attribute__((aligned(16))) char smem[2][2][TILE_BYTES];  // [buffer][K, V]
+  constexpr int BM = 32 * NW;
+  constexpr int BN = 32;
+  constexpr int KK = D / 16, NCB = D / 32;
+  constexpr int NS = 2 * KK;       // S and dP ops per tile
+  constexpr int NQ = KK;           // dQ ops per tile (2 contraction steps x NCB)
+  constexpr int RPS = 16 / NS > 0 ? 16 / NS : 1;
+  constexpr int TILE_BYTES = BN * D * 2;
+  constexpr int RING = 3;
+  __shared__ __attribute__((aligned(1024))) char kbuf[RING][TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf[RING][TILE_BYTES];
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;
@@ -271,91 +285,127 @@ __global__ __launch_bounds__(kBwdThreads, 2) void attn_bwd_dq_kernel(
   const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
 
   const size_t head_off = (size_t)bh * N * D;
-  const uint16_t* K = k + head_off;
-  const uint16_t* V = v + head_off;
+  const unsigned head_bytes = (unsigned)N * (2 * D);
+  const rsrc_t rq = make_rsrc(q + head_off, head_bytes);
+  const rsrc_t rg = make_rsrc(dout + head_off, head_bytes);
+  const rsrc_t rk = make_rsrc(k + head_off, head_bytes);
+  const rsrc_t rv = make_rsrc(v + head_off, head_bytes);
 
-  const int qrow = qt * kDqBM + wave * 32 + (lane & 31);
-  bf16x8 qf[D / 16], gf[D / 16];
+  const int qrow = qt * BM + wave * 32 + (lane & 31);
+  bf16x8 qf[KK], gf[KK];
 #pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-    if (qrow < N) {
-      a = *reinterpret_cast<const uint4*>(q + head_off + (size_t)qrow * D + 16 * kk + 8 * h);
-      b = *reinterpret_cast<const uint4*>(dout + head_off + (size_t)qrow * D + 16 * kk + 8 * h);
-    }
-    qf[kk] = as_bf16x8(a);
-    gf[kk] = as_bf16x8(b);
+  for (int kk = 0; kk < KK; ++kk) {
+    qf[kk] = as_bf16x8(buffer_load16(rq, qrow * (2 * D) + 32 * kk + 16 * h));
+    gf[kk] = as_bf16x8(buffer_load16(rg, qrow * (2 * D) + 32 * kk + 16 * h));
   }
-  const float lse2 = qrow < N ? lse[(size_t)bh * N + qrow] * kLog2e : INFINITY;
-  const float dval = qrow < N ? drow[(size_t)bh * N + qrow] : 0.f;
+  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * N, (unsigned)N * 4);
+  const rsrc_t rd = make_rsrc(drow + (size_t)bh * N, (unsigned)N * 4);
+  // (the b32 buffer load returns the raw bits)
+  const float l2 = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, qrow * 4, 0, 0));
+  const float dval = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, qrow * 4, 0, 0));
 
-  RowFrag<D> rf;
+  TileDma<D, BN, NW> dma;
+  dma.init(wave, lane);
+  RowFragX<D> rf;
   rf.init(lane);
-  TrFrag<D> tf;
+  TrFragX<D> tf;
   tf.init(lane);
 
-  f32x16 dqacc[D / 32];
+  f32x16 dqacc[NCB];
 #pragma unroll
-  for (int cb = 0; cb < D / 32; ++cb) dqacc[cb] = zero16();
+  for (int cb = 0; cb < NCB; ++cb) dqacc[cb] = zero16();
 
-  const int n_kt = (N + kDqBN - 1) / kDqBN;
-  TileLoader<D, kDqBN, kBwdThreads> kl, vl;
-  kl.load(K, 0, N, tid);
-  vl.load(V, 0, N, tid);
-  kl.store(smem[0][0], tid);
-  vl.store(smem[0][1], tid);
+  auto issue_tile = [&](int t) {
+    dma.issue(rk, t * BN, kbuf[t % RING]);
+    dma.issue(rv, t * BN, vbuf[t % RING]);
+  };
+  // op i of the score stream: S^T (i < KK) or dP^T (i >= KK)
+  auto read_s = [&](int slot, int i) {
+    return lds_frag_row(i < KK ? kbuf[slot] : vbuf[slot], rf.off(i % KK));
+  };
+
+  const int n_kt = (N + BN - 1) / BN;
+  issue_tile(0);
+  issue_tile(1);
+  wait_vmem();
+  __syncthreads();
+  f32x16 s, dp;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    if (i == 0) s = zero16();
+    if (i == KK) dp = zero16();
+    if (i < KK) s = mfma32(read_s(0, i), qf[i], s);
+    else dp = mfma32(read_s(0, i), gf[i - KK], dp);
+  }
   __syncthreads();
 
-  for (int t = 0; t < n_kt; ++t) {
-    const int buf = t & 1;
-    const bool more = t + 1 < n_kt;
-    if (more) {
-      kl.load(K, (t + 1) * kDqBN, N, tid);
-      vl.load(V, (t + 1) * kDqBN, N, tid);
+  auto stage = [&](auto has_next, int j) {
+    constexpr bool NEXT = decltype(has_next)::value;
+    const int cur = j % RING, nxt = (j + 1) % RING;
+    if constexpr (NEXT) issue_tile(j + 2);
+    bf16x8 dsb[2];
+    auto valu = [&](int u) {
+#pragma unroll
+      for (int rr = 0; rr < RPS; ++rr) {
+        const int r = u * RPS + rr;
+        if (r < 16) {
+          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c, -l2));
+          float g = p * (dp[r] - dval);
+          pin(g);
+          dp[r] = g;
+          if ((r & 7) == 7) dsb[r >> 3] = acc_to_operand(dp, r >> 3);
+        }
+      }
+    };
+    f32x16 sn, dpn;
+    if constexpr (NEXT) {
+      bf16x8 aq[2];
+      aq[0] = read_s(nxt, 0);
+      sched_fence();
+#pragma unroll
+      for (int i = 0; i < NS; ++i) {
+        if (i + 1 < NS) aq[(i + 1) & 1] = read_s(nxt, i + 1);
+        if (i == 0) sn = zero16();
+        if (i == KK) dpn = zero16();
+        if (i < KK) sn = mfma32(aq[i & 1], qf[i], sn);
+        else dpn = mfma32(aq[i & 1], gf[i - KK], dpn);
+        valu(i);
+        sched_fence();
+      }
+#pragma unroll
+      for (int i = NS; i < 16 / RPS; ++i) valu(i);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16 / RPS; ++i) valu(i);
     }
-    const char* ks = smem[buf][0];
-    const char* vs = smem[buf][1];
-    const int key0 = t * kDqBN;
-    const bool tail = key0 + kDqBN > N;
+    // dQ^T += K^T dS^T, K^T fragments read two ops ahead
+    {
+      const char* ks = kbuf[cur];
+      bf16x8 aq[2];
+      aq[0] = tf.load(ks, 0, 0);
+      sched_fence();
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) {
+        if (i + 1 < NQ) aq[(i + 1) & 1] = tf.load(ks, 16 * ((i + 1) / NCB), (i + 1) % NCB);
+        dqacc[i % NCB] = mfma32(aq[i & 1], dsb[i / NCB], dqacc[i % NCB]);
+        sched_fence();
+      }
+    }
+    if constexpr (NEXT) {
+      wait_vmem();
+      __syncthreads();
+      s = sn;
+      dp = dpn;
+    }
+  };
 
-#pragma unroll
-    for (int kb = 0; kb < kDqBN / 32; ++kb) {
-      // S^T = K Q^T, P^T = exp2(S^T c - LSE2)
-      f32x16 s = zero16();
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) s = mfma32(lds_frag_row(ks, kb * 32 * 2 * D + rf.off[kk]), qf[kk], s);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c, -lse2));
-      if (tail) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (key0 + kb * 32 + acc_row(r, h) >= N) s[r] = 0.f;
-      }
-      // dP^T = V dO^T, dS^T = P^T o (dP^T - D)
-      f32x16 dp = zero16();
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) dp = mfma32(lds_frag_row(vs, kb * 32 * 2 * D + rf.off[kk]), gf[kk], dp);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) dp[r] = s[r] * (dp[r] - dval);
-      // dQ^T += K^T dS^T
-#pragma unroll
-      for (int ks2 = 0; ks2 < 2; ++ks2) {
-        const bf16x8 df = acc_to_operand(dp, ks2);
-#pragma unroll
-        for (int cb = 0; cb < D / 32; ++cb) dqacc[cb] = mfma32(tf.load(ks, kb * 32 + 16 * ks2, cb), df, dqacc[cb]);
-      }
-    }
-    if (more) {
-      kl.store(smem[buf ^ 1][0], tid);
-      vl.store(smem[buf ^ 1][1], tid);
-    }
-    __syncthreads();
-  }
+  for (int j = 0; j < n_kt - 1; ++j) stage(std::true_type{}, j);
+  stage(std::false_type{}, n_kt - 1);
 
   if (qrow < N) {
     float* row = dq + head_off + (size_t)qrow * D;
 #pragma unroll
-    for (int cb = 0; cb < D / 32; ++cb)
+    for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
         *reinterpret_cast<float4*>(row + 32 * cb + 8 * g + 4 * h) =
@@ -393,13 +443,33 @@ VITATTN_DKDV_INSTANTIATE(128)
 VITATTN_DKDV_INSTANTIATE(64)
 #undef VITATTN_DKDV_INSTANTIATE
 
+template <int D, int NW>
+static hipError_t dq_v(const BwdArgs& a) {
+  const int n_qt = (a.N + 32 * NW - 1) / (32 * NW);
+  const int total = a.BH * n_qt;
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v, a.dout,
+                     a.drow, a.lse2, a.dq, a.N, n_qt, total, a.scale * kLog2e, a.scale);
+  return hipGetLastError();
+}
+
+#define VITATTN_DQ_INSTANTIATE(D, NW)                                                                       \
+  template __global__ void attn_bwd_dq_kernel<D, NW>(                                                      \
+      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,            \
+      const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
+      int, int, int, float, float);
+VITATTN_DQ_INSTANTIATE(128, 4)
+VITATTN_DQ_INSTANTIATE(128, 8)
+VITATTN_DQ_INSTANTIATE(64, 4)
+VITATTN_DQ_INSTANTIATE(64, 8)
+#undef VITATTN_DQ_INSTANTIATE
+
 template <int D>
 static hipError_t dq_d(const BwdArgs& a) {
-  const int n_qt = (a.N + kDqBM - 1) / kDqBM;
-  const int total = a.BH * n_qt;
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<D>, dim3(total), dim3(kBwdThreads), 0, a.stream, a.q, a.k, a.v, a.dout,
-                     a.lse, a.drow, a.dq, a.N, n_qt, total, a.scale * kLog2e, a.scale);
-  return hipGetLastError();
+  switch (tuning_variant("VITATTN_DQ_VARIANT")) {
+    case 1: return dq_v<D, 4>(a);
+    case 2: return dq_v<D, 8>(a);
+    default: return dq_v<D, 8>(a);
+  }
 }
 
 hipError_t launch_bwd_rowdot(const BwdArgs& a) { return a.d == 128 ? rowdot_d<128>(a) : rowdot_d<64>(a); }

@@ -27,6 +27,7 @@ namespace vitattn {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
@@ -107,6 +108,16 @@ struct RowFrag {
   }
 };
 
+// Same offsets from one register: chunk 2*kk + h of a row swizzled by s is
+// 2*kk ^ (h ^ s) (2*kk is even and h < 2), and the row term only has bits
+// above the chunk bits, so the offset of step kk is base ^ (32 * kk).
+template <int D>
+struct RowFragX {
+  int base;
+  __device__ __forceinline__ void init(int lane) { base = tile_off<D>(lane & 31, lane >> 5); }
+  __device__ __forceinline__ int off(int kk) const { return base ^ (32 * kk); }
+};
+
 // Transposed fragment: operand whose contraction runs along rows. For
 // contraction step base row k0 (a multiple of 16) and column block c0 (a
 // multiple of 32), lane l gets T[k0 + 8*(t/4) + 4*(l/32) + t%4][c0 + l%32]
@@ -134,6 +145,30 @@ struct TrFrag {
   __device__ __forceinline__ bf16x8 load(const char* lds, int k0, int cb) const {
     const char* p0 = lds + k0 * (2 * D) + off[0][cb];
     const char* p1 = lds + k0 * (2 * D) + off[1][cb];
+    bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
+    bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p1));
+    bf16x8 r;
+    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+    return r;
+  }
+};
+
+// TrFrag with two offset registers: column block cb moves the chunk index
+// by 4*cb, which lies in chunk bits the row swizzle XORs but no other term
+// of the offset touches, so the offset for cb is off[read] ^ (64 * cb).
+template <int D>
+struct TrFragX {
+  int off[2];
+  __device__ __forceinline__ void init(int lane) {
+    TrFrag<D> t;
+    t.init(lane);
+    off[0] = t.off[0][0];
+    off[1] = t.off[1][0];
+  }
+  __device__ __forceinline__ bf16x8 load(const char* lds, int k0, int cb) const {
+    const char* p0 = lds + k0 * (2 * D) + (off[0] ^ (64 * cb));
+    const char* p1 = lds + k0 * (2 * D) + (off[1] ^ (64 * cb));
     bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
     bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p1));
     bf16x8 r;

@@ -15,17 +15,18 @@
 // Software pipeline across tiles: the scores of tile j+1 are computed on the
 // matrix cores while the vector units turn tile j's scores into
 // probabilities. K therefore runs one tile ahead of V, in two LDS rings of
-// RING slots: iteration j reads K_{j+1} and V_j and refills the slots of K_j
-// and V_{j-1} with K_{j+RING} and V_{j+RING-1}, so every tile is requested
-// RING-1 iterations before it is used (a tile that misses in L2 then does
-// not stall the workgroup at the next barrier).
+// two slots: iteration j reads K_{j+1} and V_j and refills the slots of K_j
+// and V_{j-1} with K_{j+2} and V_{j+1}. The tile loop is unrolled by two so
+// that every LDS address is a lane offset plus a constant.
 //
 // Software pipeline within a tile: each matrix-core op's LDS operand is read
 // two ops ahead, and the softmax is cut into slices placed between the score
 // ops, with scheduling fences pinning that order (the LDS read latency is
 // then hidden behind the ops instead of stalling each of them).
 //
-// The rescale of O by exp2(m_old - m_new) is skipped when no query of the
+// The row sum adds the bf16-rounded probabilities (two per v_dot2 op), i.e.
+// exactly the weights the PV product uses. The rescale of O by
+// exp2(m_old - m_new) is skipped when no query of the
 // wave raised its running max (multiplying by 1 would change nothing), so
 // the maximum is always subtracted exactly and the largest P is exactly 1.
 #include <type_traits>
@@ -35,7 +36,7 @@
 
 namespace vitattn {
 
-template <int D, int KB, int NW, int MINW, int RING>
+template <int D, int KB, int NW, int MINW>
 __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t* __restrict__ q,
                                                                  const uint16_t* __restrict__ k,
                                                                  const uint16_t* __restrict__ v,
@@ -47,11 +48,9 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   constexpr int KK = D / 16;           // contraction steps of one 32-key score block
   constexpr int NS = KB * KK;          // score ops per tile
   constexpr int NV = 2 * KB * D / 32;  // PV ops per tile
-  constexpr int NSC = 16 * KB;         // scores per lane per tile
-  constexpr int LA = RING - 1;         // tiles requested ahead
-  static_assert(RING >= 2, "ring of at least two slots");
-  __shared__ __attribute__((aligned(1024))) char kbuf[RING][TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) char vbuf[RING][TILE_BYTES];
+  constexpr int NPAIR = 8 * KB;        // score pairs per lane per tile
+  __shared__ __attribute__((aligned(1024))) char kbuf[2][TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf[2][TILE_BYTES];
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;
@@ -82,37 +81,35 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
 #pragma unroll
   for (int cb = 0; cb < D / 32; ++cb) oacc[cb] = zero16();
   float m_run = -INFINITY;  // running max of scaled logits, log2 units
-  float l_part = 0.f;       // this lane's share of the row sum
-
-  // operand reads of the score op i (K rows) and of the PV op i (V^T)
-  auto read_k = [&](const char* ks, int i) { return lds_frag_row(ks, (i / KK) * 32 * 2 * D + kfrag.off[i % KK]); };
-  auto read_v = [&](const char* vs, int i) { return vfrag.load(vs, (i / (D / 32)) * 16, i % (D / 32)); };
+  float l_part = 0.f;       // this lane's share of the sum of the bf16 probabilities
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
   const int n_kt = (N + BN - 1) / BN;
-  // prologue: K_0 .. K_LA and V_0 .. V_{LA-1} (tiles past the end read as zeros)
-#pragma unroll
-  for (int t = 0; t < LA; ++t) {
-    dma.issue(rk, t * BN, kbuf[t]);
-    dma.issue(rv, t * BN, vbuf[t]);
-  }
-  dma.issue(rk, LA * BN, kbuf[LA]);
+  dma.issue(rk, 0, kbuf[0]);
+  dma.issue(rv, 0, vbuf[0]);
+  dma.issue(rk, BN, kbuf[1]);
   wait_vmem();
   __syncthreads();
-  f32x16 s[KB];
+  f32x16 sa[KB], sb[KB];
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
-    if (i % KK == 0) s[i / KK] = zero16();
-    s[i / KK] = mfma32(read_k(kbuf[0], i), qf[i % KK], s[i / KK]);
+    if (i % KK == 0) sa[i / KK] = zero16();
+    sa[i / KK] = mfma32(lds_frag_row(kbuf[0], (i / KK) * 32 * 2 * D + kfrag.off[i % KK]), qf[i % KK], sa[i / KK]);
   }
-  __syncthreads();  // kbuf[0] is refilled by the first iteration
+  __syncthreads();  // kbuf[0] is refilled by the first stage
 
-  // One pipeline stage: softmax and PV of tile j, scores of tile j+1.
-  auto stage = [&](auto has_next, int j) {
+  // Stage j (parity P = j & 1, known at compile time so every LDS address is
+  // a lane offset plus an immediate): softmax and PV of tile j from s, the
+  // scores of tile j+1 into sn. Reads K_{j+1} (kbuf[1-P]) and V_j (vbuf[P]);
+  // refills kbuf[P] with K_{j+2} and vbuf[1-P] with V_{j+1}.
+  auto stage = [&](auto parity, auto has_next, f32x16 (&s)[KB], f32x16 (&sn)[KB], int j) {
+    constexpr int P = decltype(parity)::value;
     constexpr bool NEXT = decltype(has_next)::value;
-    f32x16 sn[KB];
+    const char* ks = kbuf[1 - P];
+    const char* vs = vbuf[P];
     if constexpr (NEXT) {
-      dma.issue(rk, (j + 1 + LA) * BN, kbuf[(j + 1 + LA) % RING]);
-      dma.issue(rv, (j + LA) * BN, vbuf[(j + LA) % RING]);
+      dma.issue(rk, (j + 2) * BN, kbuf[P]);
+      dma.issue(rv, (j + 1) * BN, vbuf[1 - P]);
     } else {
       // the last tile may be ragged: keys past the end get -inf
       const int key0 = j * BN;
@@ -124,23 +121,22 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
             if (key0 + kb * 32 + acc_row(r, h) >= N) s[kb][r] = -INFINITY;
       }
     }
-    const char* ks = kbuf[(j + 1) % RING];
-    const char* vs = vbuf[j % RING];
 
-    // softmax state, filled slice by slice
+    // softmax of s, cut into slices: 0 and 1 reduce half of the scores each,
+    // 2 finishes the max, the rest exponentiate an equal share of the score
+    // pairs, pack them to bf16 and add them to the row sum
     float mx0 = -INFINITY, mx1 = -INFINITY, m_new = 0.f, alpha = 1.f, lsum = 0.f;
     bool raise = false;
-    // slices: 0 and 1 reduce half of the scores each; 2 finishes the max;
-    // the rest exponentiate an equal share of the scores
+    uint32_t pk[NPAIR];
     constexpr int NSLICE = NS > 3 ? NS : 4;
     auto slice = [&](int i) {
       if (i == 0) {
 #pragma unroll
-        for (int e = 0; e < NSC / 2; ++e) mx0 = fmaxf(mx0, s[e / 16][e % 16]);
+        for (int e = 0; e < 8 * KB; ++e) mx0 = fmaxf(mx0, s[e / 16][e % 16]);
         pin(mx0);
       } else if (i == 1) {
 #pragma unroll
-        for (int e = NSC / 2; e < NSC; ++e) mx1 = fmaxf(mx1, s[e / 16][e % 16]);
+        for (int e = 8 * KB; e < 16 * KB; ++e) mx1 = fmaxf(mx1, s[e / 16][e % 16]);
         pin(mx1);
       } else if (i == 2) {
         const float m_tile = max_halves(fmaxf(mx0, mx1)) * c;
@@ -151,14 +147,18 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
         pin(m_new);
       } else {
         constexpr int NE = NSLICE - 3;
-        const int e0 = (i - 3) * NSC / NE, e1 = (i - 2) * NSC / NE;
+        const int p0 = (i - 3) * NPAIR / NE, p1 = (i - 2) * NPAIR / NE;
 #pragma unroll
-        for (int e = 0; e < NSC; ++e)
-          if (e >= e0 && e < e1) {
-            float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e / 16][e % 16], c, -m_new));
-            pin(p);
-            s[e / 16][e % 16] = p;
-            lsum += p;
+        for (int pr = 0; pr < NPAIR; ++pr)
+          if (pr >= p0 && pr < p1) {
+            const int e = 2 * pr;
+            const float x0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e / 16][e % 16], c, -m_new));
+            const float x1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e / 16][e % 16 + 1], c, -m_new));
+            const bf16x2 b = {(__bf16)x0, (__bf16)x1};
+            lsum = __builtin_amdgcn_fdot2_f32_bf16(b, ones, lsum, false);
+            uint32_t u = __builtin_bit_cast(uint32_t, b);
+            asm volatile("" : "+v"(u));
+            pk[pr] = u;
           }
       }
     };
@@ -166,12 +166,12 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
     if constexpr (NEXT) {
       // scores of tile j+1 on the matrix cores, softmax of tile j in the gaps
       bf16x8 kq[3];
-      kq[0] = read_k(ks, 0);
-      kq[1] = read_k(ks, 1);
+      kq[0] = lds_frag_row(ks, kfrag.off[0]);
+      kq[1] = lds_frag_row(ks, (1 / KK) * 32 * 2 * D + kfrag.off[1 % KK]);
       sched_fence();
 #pragma unroll
       for (int i = 0; i < NS; ++i) {
-        if (i + 2 < NS) kq[(i + 2) % 3] = read_k(ks, i + 2);
+        if (i + 2 < NS) kq[(i + 2) % 3] = lds_frag_row(ks, ((i + 2) / KK) * 32 * 2 * D + kfrag.off[(i + 2) % KK]);
         if (i % KK == 0) sn[i / KK] = zero16();
         sn[i / KK] = mfma32(kq[i % 3], qf[i % KK], sn[i / KK]);
         slice(i);
@@ -186,7 +186,8 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
     l_part = l_part * alpha + lsum;
     bf16x8 pf[2 * KB];
 #pragma unroll
-    for (int ks2 = 0; ks2 < 2 * KB; ++ks2) pf[ks2] = acc_to_operand(s[ks2 >> 1], ks2 & 1);
+    for (int ks2 = 0; ks2 < 2 * KB; ++ks2)
+      pf[ks2] = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks2], pk[4 * ks2 + 1], pk[4 * ks2 + 2], pk[4 * ks2 + 3]));
     if (__any(raise)) {
 #pragma unroll
       for (int cb = 0; cb < D / 32; ++cb)
@@ -196,28 +197,36 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
     // O^T += V^T P^T, V^T fragments read two ops ahead
     {
       bf16x8 vq[3];
-      vq[0] = read_v(vs, 0);
-      vq[1] = read_v(vs, 1);
+      vq[0] = vfrag.load(vs, 0, 0);
+      vq[1] = vfrag.load(vs, 16 * (1 / (D / 32)), 1 % (D / 32));
       sched_fence();
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
-        if (i + 2 < NV) vq[(i + 2) % 3] = read_v(vs, i + 2);
+        if (i + 2 < NV) vq[(i + 2) % 3] = vfrag.load(vs, 16 * ((i + 2) / (D / 32)), (i + 2) % (D / 32));
         const int cb = i % (D / 32);
         oacc[cb] = mfma32(vq[i % 3], pf[i / (D / 32)], oacc[cb]);
         sched_fence();
       }
     }
     if constexpr (NEXT) {
-      // K_{j+2} and V_{j+1} must have landed; later requests may be in flight
-      wait_vmem_leave<(LA - 1) * 2 * decltype(dma)::PER_WAVE>();
+      wait_vmem();
       __syncthreads();
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) s[kb] = sn[kb];
     }
   };
 
-  for (int j = 0; j < n_kt - 1; ++j) stage(std::true_type{}, j);
-  stage(std::false_type{}, n_kt - 1);
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  int j = 0;
+  for (; j + 2 < n_kt; j += 2) {
+    stage(P0{}, std::true_type{}, sa, sb, j);
+    stage(P1{}, std::true_type{}, sb, sa, j + 1);
+  }
+  if (j + 1 < n_kt) {
+    stage(P0{}, std::true_type{}, sa, sb, j);
+    stage(P1{}, std::false_type{}, sb, sa, j + 1);
+  } else {
+    stage(P0{}, std::false_type{}, sa, sb, j);
+  }
 
   // epilogue: O = O^T / l (stored transposed back to [query][d]), LSE in nats.
   const float l = sum_halves(l_part);
@@ -236,13 +245,13 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   }
 }
 
-template <int D, int KB, int NW, int MINW, int RING>
+template <int D, int KB, int NW, int MINW>
 static hipError_t launch_fwd_v(const FwdArgs& a) {
   constexpr int BM = 32 * NW;
   const int n_qtiles = (a.N + BM - 1) / BM;
   const int total = a.BH * n_qtiles;
   const float c = a.scale * kLog2e;
-  hipLaunchKernelGGL((attn_fwd_kernel<D, KB, NW, MINW, RING>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v,
+  hipLaunchKernelGGL((attn_fwd_kernel<D, KB, NW, MINW>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v,
                      a.o, a.lse, a.N, n_qtiles, total, c);
   return hipGetLastError();
 }
@@ -250,31 +259,26 @@ static hipError_t launch_fwd_v(const FwdArgs& a) {
 // Every tile variant is instantiated explicitly: hipcc otherwise omits the
 // host-side launch stub of some instantiations reached only through this
 // dispatch, and the library then fails to load.
-#define VITATTN_FWD_VARIANTS(X)                                                                         \
-  X(128, 2, 8, 2, 2) X(128, 2, 8, 2, 3) X(128, 2, 8, 2, 4) X(128, 1, 4, 2, 3) X(128, 1, 4, 2, 4)     \
-      X(128, 1, 8, 2, 4) X(64, 2, 8, 2, 2) X(64, 2, 8, 2, 3) X(64, 2, 8, 2, 4) X(64, 1, 4, 2, 3)     \
-          X(64, 1, 4, 2, 4) X(64, 1, 8, 2, 4)
-#define VITATTN_FWD_INSTANTIATE(D, KB, NW, MINW, RING)                                                 \
-  template __global__ void attn_fwd_kernel<D, KB, NW, MINW, RING>(const uint16_t* __restrict__,       \
-                                                                  const uint16_t* __restrict__,       \
-                                                                  const uint16_t* __restrict__,       \
-                                                                  float* __restrict__, float* __restrict__, int, \
-                                                                  int, int, float);
+#define VITATTN_FWD_VARIANTS(X) \
+  X(128, 2, 8, 2) X(128, 2, 4, 2) X(128, 1, 8, 2) X(64, 2, 8, 2) X(64, 2, 4, 2) X(64, 1, 8, 2)
+#define VITATTN_FWD_INSTANTIATE(D, KB, NW, MINW)                                                         \
+  template __global__ void attn_fwd_kernel<D, KB, NW, MINW>(const uint16_t* __restrict__,               \
+                                                            const uint16_t* __restrict__,               \
+                                                            const uint16_t* __restrict__,               \
+                                                            float* __restrict__, float* __restrict__, int, \
+                                                            int, int, float);
 VITATTN_FWD_VARIANTS(VITATTN_FWD_INSTANTIATE)
 #undef VITATTN_FWD_INSTANTIATE
 
-// Tile variants (key blocks per tile, waves per workgroup, waves per SIMD,
-// ring slots); 0 is the default.
+// Tile variants (key blocks per tile, waves per workgroup, waves per SIMD);
+// 0 is the default.
 template <int D>
 static hipError_t launch_fwd_d(const FwdArgs& a, int variant) {
   switch (variant) {
-    case 1: return launch_fwd_v<D, 2, 8, 2, 2>(a);
-    case 2: return launch_fwd_v<D, 2, 8, 2, 3>(a);
-    case 3: return launch_fwd_v<D, 2, 8, 2, 4>(a);
-    case 4: return launch_fwd_v<D, 1, 4, 2, 3>(a);
-    case 5: return launch_fwd_v<D, 1, 4, 2, 4>(a);
-    case 6: return launch_fwd_v<D, 1, 8, 2, 4>(a);
-    default: return launch_fwd_v<D, 2, 8, 2, 3>(a);
+    case 1: return launch_fwd_v<D, 2, 8, 2>(a);
+    case 2: return launch_fwd_v<D, 2, 4, 2>(a);
+    case 3: return launch_fwd_v<D, 1, 8, 2>(a);
+    default: return launch_fwd_v<D, 2, 8, 2>(a);
   }
 }
 
