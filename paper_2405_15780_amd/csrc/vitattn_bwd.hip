@@ -256,11 +256,13 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 // One workgroup = NW waves = 32*NW query rows of one (b, h); each wave owns
 // 32 queries and keeps their Q and dO fragments (B operands), their LSE2 and
 // D and the dQ^T accumulator in registers. K and V stream through a ring of
-// three LDS slots in tiles of 32 keys. Per tile j the wave runs
+// four LDS slots in tiles of 32 keys. Per tile j the wave runs
 //   S^T = K_{j+1} Q^T and dP^T = V_{j+1} dO^T   (matrix cores)
 //     interleaved with P^T, dS^T of tile j      (vector units)
 //   dQ^T += K_j^T dS^T_j
-// Key rows past the end arrive as zeros: their P is finite and they add
+// The tile loop is unrolled by the ring depth, so slots are compile-time
+// constants and LDS addresses fold into instruction immediates. Key rows
+// past the end arrive as zeros: their P is finite and they add
 // K_row^T dS = 0 to dQ, so no masking is needed.
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
@@ -274,7 +276,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   constexpr int NQ = KK;           // dQ ops per tile (2 contraction steps x NCB)
   constexpr int RPS = 16 / NS > 0 ? 16 / NS : 1;
   constexpr int TILE_BYTES = BN * D * 2;
-  constexpr int RING = 3;
+  constexpr int RING = 4;
   __shared__ __attribute__((aligned(1024))) char kbuf[RING][TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char vbuf[RING][TILE_BYTES];
 
@@ -306,69 +308,69 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
 
   TileDma<D, BN, NW> dma;
   dma.init(wave, lane);
-  RowFragX<D> rf;
+  RowFrag<D> rf;
   rf.init(lane);
-  TrFragX<D> tf;
+  TrFrag<D> tf;
   tf.init(lane);
 
   f32x16 dqacc[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) dqacc[cb] = zero16();
 
-  auto issue_tile = [&](int t) {
-    dma.issue(rk, t * BN, kbuf[t % RING]);
-    dma.issue(rv, t * BN, vbuf[t % RING]);
-  };
-  // op i of the score stream: S^T (i < KK) or dP^T (i >= KK)
-  auto read_s = [&](int slot, int i) {
-    return lds_frag_row(i < KK ? kbuf[slot] : vbuf[slot], rf.off(i % KK));
-  };
-
   const int n_kt = (N + BN - 1) / BN;
-  issue_tile(0);
-  issue_tile(1);
+  // prologue: tiles 0 .. RING-2 requested (tiles past the end read as zeros), scores of tile 0
+#pragma unroll
+  for (int t = 0; t < RING - 1; ++t) {
+    dma.issue(rk, t * BN, kbuf[t]);
+    dma.issue(rv, t * BN, vbuf[t]);
+  }
   wait_vmem();
   __syncthreads();
-  f32x16 s, dp;
+  f32x16 sa[2], sb[2];  // [S^T, dP^T] of the current and the next tile
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
-    if (i == 0) s = zero16();
-    if (i == KK) dp = zero16();
-    if (i < KK) s = mfma32(read_s(0, i), qf[i], s);
-    else dp = mfma32(read_s(0, i), gf[i - KK], dp);
+    if (i % KK == 0) sa[i / KK] = zero16();
+    sa[i / KK] = mfma32(lds_frag_row(i < KK ? kbuf[0] : vbuf[0], rf.off[i % KK]), i < KK ? qf[i] : gf[i - KK],
+                        sa[i / KK]);
   }
-  __syncthreads();
 
-  auto stage = [&](auto has_next, int j) {
+  // Stage j with SL = j % RING known at compile time: P, dS of tile j (from
+  // s, dp) and dQ of tile j (slot SL); scores of tile j+1 (slot SL+1) into
+  // sn, dpn; tile j+RING-1 requested into the slot of tile j-1.
+  auto stage = [&](auto slot_tag, auto has_next, f32x16 (&cur)[2], f32x16 (&nxt)[2], int j) {
+    constexpr int SL = decltype(slot_tag)::value;
+    constexpr int NX = (SL + 1) % RING, RF = (SL + RING - 1) % RING;
     constexpr bool NEXT = decltype(has_next)::value;
-    const int cur = j % RING, nxt = (j + 1) % RING;
-    if constexpr (NEXT) issue_tile(j + 2);
+    if constexpr (NEXT) {
+      dma.issue(rk, (j + RING - 1) * BN, kbuf[RF]);
+      dma.issue(rv, (j + RING - 1) * BN, vbuf[RF]);
+    }
     bf16x8 dsb[2];
     auto valu = [&](int u) {
 #pragma unroll
       for (int rr = 0; rr < RPS; ++rr) {
         const int r = u * RPS + rr;
         if (r < 16) {
-          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], c, -l2));
-          float g = p * (dp[r] - dval);
+          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(cur[0][r], c, -l2));
+          float g = p * (cur[1][r] - dval);
           pin(g);
-          dp[r] = g;
-          if ((r & 7) == 7) dsb[r >> 3] = acc_to_operand(dp, r >> 3);
+          cur[1][r] = g;
+          if ((r & 7) == 7) dsb[r >> 3] = acc_to_operand(cur[1], r >> 3);
         }
       }
     };
-    f32x16 sn, dpn;
     if constexpr (NEXT) {
       bf16x8 aq[2];
-      aq[0] = read_s(nxt, 0);
+      aq[0] = lds_frag_row(kbuf[NX], rf.off[0]);
       sched_fence();
 #pragma unroll
       for (int i = 0; i < NS; ++i) {
-        if (i + 1 < NS) aq[(i + 1) & 1] = read_s(nxt, i + 1);
-        if (i == 0) sn = zero16();
-        if (i == KK) dpn = zero16();
-        if (i < KK) sn = mfma32(aq[i & 1], qf[i], sn);
-        else dpn = mfma32(aq[i & 1], gf[i - KK], dpn);
+        if (i + 1 < NS) {
+          const int n = i + 1;
+          aq[n & 1] = lds_frag_row(n < KK ? kbuf[NX] : vbuf[NX], rf.off[n % KK]);
+        }
+        if (i % KK == 0) nxt[i / KK] = zero16();
+        nxt[i / KK] = mfma32(aq[i & 1], i < KK ? qf[i] : gf[i - KK], nxt[i / KK]);
         valu(i);
         sched_fence();
       }
@@ -378,9 +380,9 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
 #pragma unroll
       for (int i = 0; i < 16 / RPS; ++i) valu(i);
     }
-    // dQ^T += K^T dS^T, K^T fragments read two ops ahead
+    // dQ^T += K^T dS^T, K^T fragments read one op ahead
     {
-      const char* ks = kbuf[cur];
+      const char* ks = kbuf[SL];
       bf16x8 aq[2];
       aq[0] = tf.load(ks, 0, 0);
       sched_fence();
@@ -392,15 +394,33 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
       }
     }
     if constexpr (NEXT) {
-      wait_vmem();
+      // tile j+2 must have landed; tile j+3 may still be in flight
+      wait_vmem_leave<2 * decltype(dma)::PER_WAVE>();
       __syncthreads();
-      s = sn;
-      dp = dpn;
     }
   };
 
-  for (int j = 0; j < n_kt - 1; ++j) stage(std::true_type{}, j);
-  stage(std::false_type{}, n_kt - 1);
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  using Y = std::true_type;
+  using F = std::false_type;
+  // The tile count is rounded up to a multiple of the ring depth: the extra
+  // tiles are all zero rows and add exactly nothing to dQ (see above), and
+  // every stage then has a compile-time slot.
+  const int n_iter = (n_kt + RING - 1) / RING * RING;
+  int j = 0;
+  for (; j + RING < n_iter; j += RING) {
+    stage(S0{}, Y{}, sa, sb, j);
+    stage(S1{}, Y{}, sb, sa, j + 1);
+    stage(S2{}, Y{}, sa, sb, j + 2);
+    stage(S3{}, Y{}, sb, sa, j + 3);
+  }
+  stage(S0{}, Y{}, sa, sb, j);
+  stage(S1{}, Y{}, sb, sa, j + 1);
+  stage(S2{}, Y{}, sa, sb, j + 2);
+  stage(S3{}, F{}, sb, sa, j + 3);
 
   if (qrow < N) {
     float* row = dq + head_off + (size_t)qrow * D;
