@@ -78,7 +78,10 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 // tiles of 64 queries (two blocks of 32); in iteration t role P works on
 // tile t and role dS on tile t-1, and tile t+1 is being fetched. Query rows
 // past the end arrive as zeros and then contribute exactly nothing (P =
-// exp2(0) = 1 multiplies dO = 0, and dS = P (dP - D) = 0).
+// exp2(0) = 1 multiplies dO = 0, and dS = P (dP - D) = 0), so the tile count
+// is rounded up until the middle iterations group into threes, and every
+// slot index is then a compile-time constant (LDS addresses fold into
+// instruction immediates).
 //
 // Each wave's work per tile is one stream of 4*D/16 matrix-core ops whose
 // LDS operands are read two ops ahead, in four phases (query blocks 0, 1):
@@ -101,8 +104,8 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   __shared__ __attribute__((aligned(1024))) char qbuf[RING][TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char gbuf[RING][TILE_BYTES];
   __shared__ __attribute__((aligned(16))) float sbuf[RING][2 * kDkvBQ];  // [D | LSE2]
-  // P exchange: [buffer][key block][query block][contraction step][lane] of 8 bf16
-  __shared__ __attribute__((aligned(16))) uint4 xbuf[2][kBwdWaves][2][2][64];
+  // P exchange: [slot][key block][query block][contraction step][lane] of 8 bf16
+  __shared__ __attribute__((aligned(16))) uint4 xbuf[RING][kBwdWaves][2][2][64];
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_ktiles;
@@ -138,21 +141,21 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero16();
 
-  auto issue_tile = [&](int t) {
-    const int slot = t % RING;
-    dma.issue(rq, t * kDkvBQ, qbuf[slot]);
-    dma.issue(rg, t * kDkvBQ, gbuf[slot]);
-    stats_dma(rd, rl, t * kDkvBQ, sbuf[slot], lane);
+  auto issue_tile = [&](auto slot_tag, int t) {
+    constexpr int SL = decltype(slot_tag)::value;
+    dma.issue(rq, t * kDkvBQ, qbuf[SL]);
+    dma.issue(rg, t * kDkvBQ, gbuf[SL]);
+    stats_dma(rd, rl, t * kDkvBQ, sbuf[SL], lane);
   };
 
-  // One tile of one role. ROLE_P: S/P/dV on tile t; otherwise dP/dS/dK.
-  auto run_tile = [&](auto role_tag, int t) {
+  // One tile of one role, in ring slot SL. Role P: S/P/dV; role dS: dP/dS/dK.
+  auto run_tile = [&](auto role_tag, auto slot_tag) {
     constexpr bool RP = decltype(role_tag)::value;
-    const int slot = t % RING;
-    const char* qs = qbuf[slot];
-    const char* gs = gbuf[slot];
-    const float* st = sbuf[slot];
-    uint4(*xb)[2][64] = xbuf[t & 1][kb];
+    constexpr int SL = decltype(slot_tag)::value;
+    const char* qs = qbuf[SL];
+    const char* gs = gbuf[SL];
+    const float* st = sbuf[SL];
+    uint4(*xb)[2][64] = xbuf[SL][kb];
 
     f32x16 m1[2];          // S (P) or dP (dS), per query block
     bf16x8 ob[2][2];       // bf16 operands of P or dS [block][contraction step]
@@ -223,20 +226,37 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     }
   };
 
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using RoleP = std::true_type;
+  using RoleDs = std::false_type;
+  // Iteration t: role P on tile t (slot t % 3), role dS on tile t-1, tile t+1
+  // requested into slot (t+1) % 3. Rounding the tile count to 1 mod 3 lets
+  // iterations 1 .. n_pad-1 run in groups of three with fixed slots.
   const int n_qt = (N + kDkvBQ - 1) / kDkvBQ;
-  issue_tile(0);
-  wait_vmem();
-  __syncthreads();
-  for (int t = 0; t <= n_qt; ++t) {
-    if (t + 1 < n_qt) issue_tile(t + 1);
+  const int n_pad = n_qt + (3 + 1 - n_qt % 3) % 3;
+  auto iteration = [&](auto slot_p, auto slot_next, auto slot_ds, int t, bool do_p, bool do_ds) {
+    issue_tile(slot_next, t + 1);  // past the end: zero rows, never read
     if (role_p) {
-      if (t < n_qt) run_tile(std::true_type{}, t);
+      if (do_p) run_tile(RoleP{}, slot_p);
     } else {
-      if (t >= 1) run_tile(std::false_type{}, t - 1);
+      if (do_ds) run_tile(RoleDs{}, slot_ds);
     }
     wait_vmem();
     __syncthreads();
+  };
+  issue_tile(S0{}, 0);
+  wait_vmem();
+  __syncthreads();
+  iteration(S0{}, S1{}, S2{}, 0, true, false);
+  for (int t = 1; t < n_pad; t += 3) {
+    iteration(S1{}, S2{}, S0{}, t, true, true);
+    iteration(S2{}, S0{}, S1{}, t + 1, true, true);
+    iteration(S0{}, S1{}, S2{}, t + 2, true, true);
   }
+  // last: role dS on tile n_pad-1 (slot 0, since n_pad = 1 mod 3)
+  if (!role_p) run_tile(RoleDs{}, S0{});
   (void)DMA_PER_TILE;
 
   if (key < N) {
