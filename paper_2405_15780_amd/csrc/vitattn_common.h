@@ -23,12 +23,15 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace vitattn {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -235,6 +238,7 @@ struct TileDma {
   static constexpr int INSTR = R * CH / 64;  // wave instructions per tile
   static constexpr int PER_WAVE = INSTR >= NW ? INSTR / NW : 1;
   static_assert(INSTR % NW == 0 || NW % INSTR == 0, "tile must divide evenly among waves");
+  static constexpr bool ALL_ACTIVE = INSTR >= NW;  // every wave has a share
   int voff[PER_WAVE];  // byte offset of this lane's chunk relative to row0
   int lds_off;         // LDS byte offset of this wave's first instruction
   bool active;         // false for waves left without work on small tiles
@@ -250,8 +254,14 @@ struct TileDma {
     lds_off = (wave * PER_WAVE) % INSTR * 1024;
     active = wave * PER_WAVE < INSTR;
   }
+  // Instruction i (< PER_WAVE) of this wave's share of the tile.
+  __device__ __forceinline__ void issue_one(rsrc_t r, int row0, char* lds_tile, int i) const {
+    if (!ALL_ACTIVE && !active) return;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(lds_tile + lds_off + i * 1024), 16,
+                                             row0 * (2 * D) + voff[i], 0, 0, 0);
+  }
   __device__ __forceinline__ void issue(rsrc_t r, int row0, char* lds_tile) const {
-    if (!active) return;
+    if (!ALL_ACTIVE && !active) return;
     const int base = row0 * (2 * D);
 #pragma unroll
     for (int i = 0; i < PER_WAVE; ++i)
@@ -278,5 +288,16 @@ __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0
 // Force a value to be computed before this point (IR passes otherwise sink
 // pure arithmetic such as exp2 past the fences, towards its first use).
 __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
+
+// f(integral_constant<int, I>) for I = B .. E-1, each call inlined with I a
+// compile-time constant (a plain unrolled loop leaves the index to the
+// unroller, and large bodies then fall back to run-time indexing).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 }  // namespace vitattn

@@ -36,6 +36,16 @@
 
 namespace vitattn {
 
+// Score e (of 16*KB per lane) is exponentiated in slot e*W/(16*KB); the
+// probabilities of 16-key step t (scores 8t .. 8t+7) are consumed by the PV
+// op at NS + CPB*t and must be complete two slots earlier.
+constexpr bool exp_schedule_ok(int NS, int CPB, int KB, int W) {
+  const int ne = 16 * KB;
+  for (int t = 0; t < 2 * KB; ++t)
+    if ((8 * t + 7) * W / ne > NS + CPB * t - 2) return false;
+  return true;
+}
+
 template <int D, int KB, int NW, int MINW>
 __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t* __restrict__ q,
                                                                  const uint16_t* __restrict__ k,
@@ -90,127 +100,156 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   dma.issue(rk, BN, kbuf[1]);
   wait_vmem();
   __syncthreads();
+
+  constexpr int NE = 16 * KB;  // scores per lane per tile
+  // keys past the end arrive as zeros; their scores become -inf
+  auto mask_ragged = [&](f32x16 (&s)[KB], int tile) {
+    const int key0 = tile * BN;
+    if (key0 + BN > N) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (key0 + kb * 32 + acc_row(r, h) >= N) s[kb][r] = -INFINITY;
+    }
+  };
+  // lane-local maximum of quarter q of a tile's scores
+  auto max_quarter = [&](const f32x16 (&s)[KB], int q) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int e = q * NE / 4; e < (q + 1) * NE / 4; ++e) m = fmaxf(m, s[e / 16][e % 16]);
+    return m;
+  };
+  // fold a tile's lane-local maximum into the running max (log2 units);
+  // alpha rescales what was accumulated against the old max
+  float alpha = 1.f;
+  bool raise = false;
+  auto max_finish = [&](float mx) {
+    const float m_tile = max_halves(mx) * c;
+    raise = m_tile > m_run;
+    const float m_new = fmaxf(m_run, m_tile);
+    alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+  };
+
   f32x16 sa[KB], sb[KB];
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
     if (i % KK == 0) sa[i / KK] = zero16();
     sa[i / KK] = mfma32(lds_frag_row(kbuf[0], (i / KK) * 32 * 2 * D + kfrag.off[i % KK]), qf[i % KK], sa[i / KK]);
   }
+  if (n_kt == 1) mask_ragged(sa, 0);
+  max_finish(fmaxf(fmaxf(max_quarter(sa, 0), max_quarter(sa, 1)), fmaxf(max_quarter(sa, 2), max_quarter(sa, 3))));
   __syncthreads();  // kbuf[0] is refilled by the first stage
 
   // Stage j (parity P = j & 1, known at compile time so every LDS address is
-  // a lane offset plus an immediate): softmax and PV of tile j from s, the
-  // scores of tile j+1 into sn. Reads K_{j+1} (kbuf[1-P]) and V_j (vbuf[P]);
-  // refills kbuf[P] with K_{j+2} and vbuf[1-P] with V_{j+1}.
+  // a lane offset plus an immediate). On entry s holds tile j's scores and
+  // m_run already covers them. One stream of NS score ops (tile j+1, into
+  // sn) then NV PV ops (tile j), each with its LDS operand read two ops
+  // ahead; the vector work rides along: the exponentials of tile j spread
+  // over the stream (the probabilities of 16-key step t are complete two ops
+  // before the PV op that uses them), this wave's DMA requests for K_{j+2}
+  // and V_{j+1} on the first odd slots, and the maximum of tile j+1 in the
+  // last slots. Reads K_{j+1} (kbuf[1-P]) and V_j (vbuf[P]); refills kbuf[P]
+  // and vbuf[1-P].
   auto stage = [&](auto parity, auto has_next, f32x16 (&s)[KB], f32x16 (&sn)[KB], int j) {
     constexpr int P = decltype(parity)::value;
     constexpr bool NEXT = decltype(has_next)::value;
+    constexpr int CPB = D / 32;  // PV ops per 16-key step
     const char* ks = kbuf[1 - P];
     const char* vs = vbuf[P];
-    if constexpr (NEXT) {
-      dma.issue(rk, (j + 2) * BN, kbuf[P]);
-      dma.issue(rv, (j + 1) * BN, vbuf[1 - P]);
-    } else {
-      // the last tile may be ragged: keys past the end get -inf
-      const int key0 = j * BN;
-      if (key0 + BN > N) {
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (key0 + kb * 32 + acc_row(r, h) >= N) s[kb][r] = -INFINITY;
-      }
-    }
-
-    // softmax of s, cut into slices: 0 and 1 reduce half of the scores each,
-    // 2 finishes the max, the rest exponentiate an equal share of the score
-    // pairs, pack them to bf16 and add them to the row sum
-    float mx0 = -INFINITY, mx1 = -INFINITY, m_new = 0.f, alpha = 1.f, lsum = 0.f;
-    bool raise = false;
-    uint32_t pk[NPAIR];
-    constexpr int NSLICE = NS > 3 ? NS : 4;
-    auto slice = [&](int i) {
-      if (i == 0) {
-#pragma unroll
-        for (int e = 0; e < 8 * KB; ++e) mx0 = fmaxf(mx0, s[e / 16][e % 16]);
-        pin(mx0);
-      } else if (i == 1) {
-#pragma unroll
-        for (int e = 8 * KB; e < 16 * KB; ++e) mx1 = fmaxf(mx1, s[e / 16][e % 16]);
-        pin(mx1);
-      } else if (i == 2) {
-        const float m_tile = max_halves(fmaxf(mx0, mx1)) * c;
-        raise = m_tile > m_run;
-        m_new = fmaxf(m_run, m_tile);
-        alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        pin(m_new);
-      } else {
-        constexpr int NE = NSLICE - 3;
-        const int p0 = (i - 3) * NPAIR / NE, p1 = (i - 2) * NPAIR / NE;
-#pragma unroll
-        for (int pr = 0; pr < NPAIR; ++pr)
-          if (pr >= p0 && pr < p1) {
-            const int e = 2 * pr;
-            const float x0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e / 16][e % 16], c, -m_new));
-            const float x1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e / 16][e % 16 + 1], c, -m_new));
-            const bf16x2 b = {(__bf16)x0, (__bf16)x1};
+    const float m_cur = m_run;
+    float lsum = 0.f;
+    u32x4 pq[2 * KB];  // bf16 P^T operands, four pairs per 16-key step
+    float xe[NE];
+    // exponentials of the scores e with first + e*W/NE == i
+    auto exp_slice = [&](auto I, auto WC) __attribute__((always_inline)) {
+      constexpr int i = decltype(I)::value;
+      constexpr int W = decltype(WC)::value;
+      static_for<0, NE>([&](auto EC) __attribute__((always_inline)) {
+        constexpr int e = decltype(EC)::value;
+        if constexpr (e * W / NE == i) {
+          xe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e / 16][e % 16], c, -m_cur));
+          if constexpr ((e & 1) != 0) {
+            const bf16x2 b = {(__bf16)xe[e - 1], (__bf16)xe[e]};
             lsum = __builtin_amdgcn_fdot2_f32_bf16(b, ones, lsum, false);
-            uint32_t u = __builtin_bit_cast(uint32_t, b);
-            asm volatile("" : "+v"(u));
-            pk[pr] = u;
+            pin(lsum);  // keeps the exponentials and the packing in this slice
+            constexpr int pr = e / 2;
+            pq[pr / 4][pr % 4] = __builtin_bit_cast(uint32_t, b);
           }
-      }
+        }
+      });
     };
+    auto pfrag = [&](int t) { return __builtin_bit_cast(bf16x8, pq[t]); };
 
     if constexpr (NEXT) {
-      // scores of tile j+1 on the matrix cores, softmax of tile j in the gaps
-      bf16x8 kq[3];
-      kq[0] = lds_frag_row(ks, kfrag.off[0]);
-      kq[1] = lds_frag_row(ks, (1 / KK) * 32 * 2 * D + kfrag.off[1 % KK]);
+      constexpr int NOPS = NS + NV;
+      constexpr int W = NOPS - 5;  // exponentials in slots 0 .. W-1
+      static_assert(exp_schedule_ok(NS, CPB, KB, W), "probabilities must be ready before their PV op");
+      constexpr int NDMA = 2 * decltype(dma)::PER_WAVE;
+      static_assert(2 * NDMA - 1 < NOPS, "DMA requests must fit the stream");
+      // score op i: key block i % KB, contraction step i / KB (the KB
+      // accumulator chains are interleaved, so consecutive ops are independent)
+      auto load_op = [&](int i) -> bf16x8 {
+        if (i < NS) return lds_frag_row(ks, (i % KB) * 32 * 2 * D + kfrag.off[i / KB]);
+        const int t = i - NS;
+        return vfrag.load(vs, 16 * (t / CPB), t % CPB);
+      };
+      float mq[4];
+      bf16x8 opq[3];
+      opq[0] = load_op(0);
+      opq[1] = load_op(1);
       sched_fence();
-#pragma unroll
-      for (int i = 0; i < NS; ++i) {
-        if (i + 2 < NS) kq[(i + 2) % 3] = lds_frag_row(ks, ((i + 2) / KK) * 32 * 2 * D + kfrag.off[(i + 2) % KK]);
-        if (i % KK == 0) sn[i / KK] = zero16();
-        sn[i / KK] = mfma32(kq[i % 3], qf[i % KK], sn[i / KK]);
-        slice(i);
+      static_for<0, NOPS>([&](auto IC) __attribute__((always_inline)) {
+        constexpr int i = decltype(IC)::value;
+        if constexpr (i + 2 < NOPS) opq[(i + 2) % 3] = load_op(i + 2);
+        if constexpr (i < NS) {
+          if constexpr (i / KB == 0) sn[i % KB] = zero16();
+          sn[i % KB] = mfma32(opq[i % 3], qf[i / KB], sn[i % KB]);
+        } else {
+          constexpr int t = i - NS;
+          oacc[t % CPB] = mfma32(opq[i % 3], pfrag(t / CPB), oacc[t % CPB]);
+        }
+        if constexpr ((i & 1) == 1 && i / 2 < NDMA) {
+          constexpr int q = i / 2, PW = NDMA / 2;
+          if constexpr (q < PW)
+            dma.issue_one(rk, (j + 2) * BN, kbuf[P], q);
+          else
+            dma.issue_one(rv, (j + 1) * BN, vbuf[1 - P], q - PW);
+        }
+        exp_slice(IC, std::integral_constant<int, W>{});
+        if constexpr (i >= W && i < W + 4) {
+          if constexpr (i == W) mask_ragged(sn, j + 1);
+          mq[i - W] = max_quarter(sn, i - W);
+          pin(mq[i - W]);
+        }
         sched_fence();
+      });
+      l_part += lsum;
+      max_finish(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3])));
+      l_part *= alpha;
+      if (__any(raise)) {
+#pragma unroll
+        for (int cb = 0; cb < D / 32; ++cb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
       }
-#pragma unroll
-      for (int i = NS; i < NSLICE; ++i) slice(i);
+      wait_vmem();
+      __syncthreads();
     } else {
-#pragma unroll
-      for (int i = 0; i < NSLICE; ++i) slice(i);
-    }
-    l_part = l_part * alpha + lsum;
-    bf16x8 pf[2 * KB];
-#pragma unroll
-    for (int ks2 = 0; ks2 < 2 * KB; ++ks2)
-      pf[ks2] = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks2], pk[4 * ks2 + 1], pk[4 * ks2 + 2], pk[4 * ks2 + 3]));
-    if (__any(raise)) {
-#pragma unroll
-      for (int cb = 0; cb < D / 32; ++cb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
-    }
-    // O^T += V^T P^T, V^T fragments read two ops ahead
-    {
+      // last tile: all exponentials, then O^T += V^T P^T
+      exp_slice(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{});
       bf16x8 vq[3];
       vq[0] = vfrag.load(vs, 0, 0);
-      vq[1] = vfrag.load(vs, 16 * (1 / (D / 32)), 1 % (D / 32));
+      vq[1] = vfrag.load(vs, 16 * (1 / CPB), 1 % CPB);
       sched_fence();
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
-        if (i + 2 < NV) vq[(i + 2) % 3] = vfrag.load(vs, 16 * ((i + 2) / (D / 32)), (i + 2) % (D / 32));
-        const int cb = i % (D / 32);
-        oacc[cb] = mfma32(vq[i % 3], pf[i / (D / 32)], oacc[cb]);
+        if (i + 2 < NV) vq[(i + 2) % 3] = vfrag.load(vs, 16 * ((i + 2) / CPB), (i + 2) % CPB);
+        oacc[i % CPB] = mfma32(vq[i % 3], pfrag(i / CPB), oacc[i % CPB]);
         sched_fence();
       }
-    }
-    if constexpr (NEXT) {
-      wait_vmem();
-      __syncthreads();
+      l_part += lsum;
     }
   };
 
