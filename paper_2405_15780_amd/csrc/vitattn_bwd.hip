@@ -101,9 +101,21 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   constexpr int TILE_BYTES = kDkvBQ * D * 2;
   constexpr int RING = 3;
   constexpr int NWAVES = 2 * kBwdWaves;
-  __shared__ __attribute__((aligned(1024))) char qbuf[RING][TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) char gbuf[RING][TILE_BYTES];
-  __shared__ __attribute__((aligned(16))) float sbuf[RING][2 * kDkvBQ];  // [D | LSE2]
+  // One variable per ring slot: the compiler then knows that reading one
+  // slot never overlaps the DMA into another and inserts no wait for it.
+  __shared__ __attribute__((aligned(1024))) char qbuf0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char qbuf1[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char qbuf2[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char gbuf0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char gbuf1[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char gbuf2[TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) float sbuf0[2 * kDkvBQ];  // [D | LSE2]
+  __shared__ __attribute__((aligned(16))) float sbuf1[2 * kDkvBQ];
+  __shared__ __attribute__((aligned(16))) float sbuf2[2 * kDkvBQ];
+  static_assert(RING == 3, "one variable per slot");
+  char* const qbuf[RING] = {qbuf0, qbuf1, qbuf2};
+  char* const gbuf[RING] = {gbuf0, gbuf1, gbuf2};
+  float* const sbuf[RING] = {sbuf0, sbuf1, sbuf2};
   // P exchange: [slot][key block][query block][contraction step][lane] of 8 bf16
   __shared__ __attribute__((aligned(16))) uint4 xbuf[RING][kBwdWaves][2][2][64];
 
@@ -149,7 +161,10 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   };
 
   // One tile of one role, in ring slot SL. Role P: S/P/dV; role dS: dP/dS/dK.
-  auto run_tile = [&](auto role_tag, auto slot_tag) {
+  // The row statistics (and role dS's P) of both query blocks are read
+  // before `prefetch` requests the next tile, so that none of these LDS
+  // reads has to wait for that DMA.
+  auto run_tile = [&](auto role_tag, auto slot_tag, auto&& prefetch) {
     constexpr bool RP = decltype(role_tag)::value;
     constexpr int SL = decltype(slot_tag)::value;
     const char* qs = qbuf[SL];
@@ -196,10 +211,13 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       }
     };
 
+    read_side(0);
+    read_side(1);
     bf16x8 aq[3];
     aq[0] = read_a(0);
     aq[1] = read_a(1);
-    read_side(0);
+    sched_fence();
+    prefetch();
     sched_fence();
 #pragma unroll
     for (int i = 0; i < NOPS; ++i) {
@@ -208,10 +226,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       if (ph < 2) {
         if (j == 0) m1[qb] = zero16();
         m1[qb] = mfma32(aq[i % 3], hf[j], m1[qb]);
-        if (ph == 1) {
-          if (j == 0) read_side(1);
-          valu(0, j);
-        }
+        if (ph == 1) valu(0, j);
       } else {
         acc[j % NCB] = mfma32(aq[i % 3], ob[qb][j / NCB], acc[j % NCB]);
         if (ph == 2) valu(1, j);
@@ -237,11 +252,14 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   const int n_qt = (N + kDkvBQ - 1) / kDkvBQ;
   const int n_pad = n_qt + (3 + 1 - n_qt % 3) % 3;
   auto iteration = [&](auto slot_p, auto slot_next, auto slot_ds, int t, bool do_p, bool do_ds) {
-    issue_tile(slot_next, t + 1);  // past the end: zero rows, never read
+    // tile t+1 past the end: zero rows, never read
+    auto prefetch = [&]() { issue_tile(slot_next, t + 1); };
     if (role_p) {
-      if (do_p) run_tile(RoleP{}, slot_p);
+      if (do_p) run_tile(RoleP{}, slot_p, prefetch);
+      else prefetch();
     } else {
-      if (do_ds) run_tile(RoleDs{}, slot_ds);
+      if (do_ds) run_tile(RoleDs{}, slot_ds, prefetch);
+      else prefetch();
     }
     wait_vmem();
     __syncthreads();
@@ -256,7 +274,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     iteration(S0{}, S1{}, S2{}, t + 2, true, true);
   }
   // last: role dS on tile n_pad-1 (slot 0, since n_pad = 1 mod 3)
-  if (!role_p) run_tile(RoleDs{}, S0{});
+  if (!role_p) run_tile(RoleDs{}, S0{}, [] {});
   (void)DMA_PER_TILE;
 
   if (key < N) {
@@ -297,8 +315,19 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   constexpr int RPS = 16 / NS > 0 ? 16 / NS : 1;
   constexpr int TILE_BYTES = BN * D * 2;
   constexpr int RING = 4;
-  __shared__ __attribute__((aligned(1024))) char kbuf[RING][TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) char vbuf[RING][TILE_BYTES];
+  // One variable per ring slot (no wait for reads of one slot while the DMA
+  // into another is in flight).
+  __shared__ __attribute__((aligned(1024))) char kbuf0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char kbuf1[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char kbuf2[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char kbuf3[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf1[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf2[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf3[TILE_BYTES];
+  static_assert(RING == 4, "one variable per slot");
+  char* const kbuf[RING] = {kbuf0, kbuf1, kbuf2, kbuf3};
+  char* const vbuf[RING] = {vbuf0, vbuf1, vbuf2, vbuf3};
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;

@@ -19,16 +19,20 @@
 // and V_{j-1} with K_{j+2} and V_{j+1}. The tile loop is unrolled by two so
 // that every LDS address is a lane offset plus a constant.
 //
-// Software pipeline within a tile: each matrix-core op's LDS operand is read
-// two ops ahead, and the softmax is cut into slices placed between the score
-// ops, with scheduling fences pinning that order (the LDS read latency is
-// then hidden behind the ops instead of stalling each of them).
+// Software pipeline within a tile: one stream of score ops then PV ops, each
+// op's LDS operand read two ops ahead, with the vector work cut into slices
+// placed between the ops and scheduling fences pinning that order. The
+// matrix cores only stay busy while each wave's vector work is spread thinly
+// and evenly over its own op stream, so the exponentials of tile j cover both
+// the score ops of tile j+1 and the PV ops of tile j (each 16-key step's
+// probabilities finish two ops before the PV op that reads them), and the
+// row max of tile j+1 is taken in the last PV slots.
 //
-// The row sum adds the bf16-rounded probabilities (two per v_dot2 op), i.e.
-// exactly the weights the PV product uses. The rescale of O by
-// exp2(m_old - m_new) is skipped when no query of the
-// wave raised its running max (multiplying by 1 would change nothing), so
-// the maximum is always subtracted exactly and the largest P is exactly 1.
+// The row sum adds the fp32 probabilities in two partial sums (plain adds:
+// a v_dot2 over the bf16 pairs would compete with the matrix cores). The
+// rescale of O by exp2(m_old - m_new) is skipped when no query of the wave
+// raised its running max (multiplying by 1 would change nothing), so the
+// maximum is always subtracted exactly and the largest P is exactly 1.
 #include <type_traits>
 
 #include "vitattn_common.h"
@@ -59,8 +63,14 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   constexpr int NS = KB * KK;          // score ops per tile
   constexpr int NV = 2 * KB * D / 32;  // PV ops per tile
   constexpr int NPAIR = 8 * KB;        // score pairs per lane per tile
-  __shared__ __attribute__((aligned(1024))) char kbuf[2][TILE_BYTES];
-  __shared__ __attribute__((aligned(1024))) char vbuf[2][TILE_BYTES];
+  // One variable per ring slot: the compiler then knows that reading one
+  // slot never overlaps the DMA into another and inserts no wait for it.
+  __shared__ __attribute__((aligned(1024))) char kbuf0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char kbuf1[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf0[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf1[TILE_BYTES];
+  char* const kbuf[2] = {kbuf0, kbuf1};
+  char* const vbuf[2] = {vbuf0, vbuf1};
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;
@@ -92,7 +102,6 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   for (int cb = 0; cb < D / 32; ++cb) oacc[cb] = zero16();
   float m_run = -INFINITY;  // running max of scaled logits, log2 units
   float l_part = 0.f;       // this lane's share of the sum of the bf16 probabilities
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
   const int n_kt = (N + BN - 1) / BN;
   dma.issue(rk, 0, kbuf[0]);
@@ -159,7 +168,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
     const char* ks = kbuf[1 - P];
     const char* vs = vbuf[P];
     const float m_cur = m_run;
-    float lsum = 0.f;
+    float ls0 = 0.f, ls1 = 0.f;
     u32x4 pq[2 * KB];  // bf16 P^T operands, four pairs per 16-key step
     float xe[NE];
     // exponentials of the scores e with first + e*W/NE == i
@@ -172,8 +181,10 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
           xe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e / 16][e % 16], c, -m_cur));
           if constexpr ((e & 1) != 0) {
             const bf16x2 b = {(__bf16)xe[e - 1], (__bf16)xe[e]};
-            lsum = __builtin_amdgcn_fdot2_f32_bf16(b, ones, lsum, false);
-            pin(lsum);  // keeps the exponentials and the packing in this slice
+            ls0 += xe[e - 1];
+            ls1 += xe[e];
+            pin(ls0);  // keep the exponentials in this slice
+            pin(ls1);
             constexpr int pr = e / 2;
             pq[pr / 4][pr % 4] = __builtin_bit_cast(uint32_t, b);
           }
@@ -225,7 +236,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
         }
         sched_fence();
       });
-      l_part += lsum;
+      l_part += ls0 + ls1;
       max_finish(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3])));
       l_part *= alpha;
       if (__any(raise)) {
@@ -249,7 +260,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
         oacc[i % CPB] = mfma32(vq[i % 3], pfrag(i / CPB), oacc[i % CPB]);
         sched_fence();
       }
-      l_part += lsum;
+      l_part += ls0 + ls1;
     }
   };
 
