@@ -13,7 +13,11 @@ Prints one JSON line. `roofline` describes the kernel with the largest share
 of the step time, timed with HIP events on the stream it is launched on
 (PyTorch's current stream, which the binding passes to the library).
 `cpu_baseline` times the fp64 oracle on a bounded slice of the same workload
-(a block of query rows of head 0, forward plus that block's backward work).
+(a block of query rows of head 0, forward plus that block's backward work)
+and extrapolates it, labelled as such, to the whole workload. `clock` holds
+the graphics clock and socket power amd-smi read during the timed steps and
+the percentage of the dense bf16 peak at that clock (the chip holds well
+below its 2.4 GHz peak clock under this load).
 """
 import argparse
 import json
@@ -31,8 +35,8 @@ PEAK_HBM_GBS = 8000.0
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=5)
-    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--config", type=int, default=4, help="workload id (4 = B1 H2 N188416 d128)")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -83,6 +87,70 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 3}), flush=True)
 
 
+class SmiSampler:
+    """Samples socket power and the graphics clock with `amd-smi metric -p -c`
+    in a background thread (about every 0.25 s) while the timed loop runs.
+    Reports nothing if amd-smi is missing or prints something unexpected."""
+
+    def __init__(self):
+        import shutil
+        import threading
+
+        self.exe = shutil.which("amd-smi")
+        self.samples = []
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        import re
+        import subprocess
+
+        while not self._stop.is_set():
+            try:
+                out = subprocess.run([self.exe, "metric", "-p", "-c"], capture_output=True, text=True,
+                                     timeout=5).stdout
+            except Exception:  # sampling is best effort
+                return
+            pw = re.search(r"SOCKET_POWER:\s*([0-9.]+)\s*W", out)
+            clk = re.search(r"GFX_0:\s*\n\s*CLK:\s*([0-9.]+)\s*MHz", out)
+            if pw and clk:
+                self.samples.append((float(pw.group(1)), float(clk.group(1))))
+            self._stop.wait(0.25)
+
+    def __enter__(self):
+        if self.exe:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self.exe and self._thread.is_alive():
+            self._thread.join(timeout=10)
+
+    def summary(self):
+        if not self.samples:
+            return None
+        import statistics
+
+        # drop readings taken while the GPU was still idle or ramping
+        busy = [(p, c) for p, c in self.samples if c >= 500.0] or self.samples
+        pw = [p for p, _ in busy]
+        clk = [c for _, c in busy]
+        return {"samples": len(busy), "power_w_median": statistics.median(pw),
+                "sclk_mhz_median": statistics.median(clk), "sclk_mhz_min": min(clk), "sclk_mhz_max": max(clk)}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(w, x, budget_s):
     import numpy as np
 
@@ -103,6 +171,7 @@ def cpu_baseline(w, x, budget_s):
         done = r1
     dt = time.perf_counter() - t0
     flops = 14.0 * done * w.N * w.d if w.backward else 4.0 * done * w.N * w.d
+    rows_total = w.B * w.H * w.N
     return {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
@@ -111,7 +180,11 @@ def cpu_baseline(w, x, budget_s):
         "sample": f"fp64 forward+backward of query rows 0..{done - 1} of head 0 against all {w.N} keys "
                   f"({done}/{w.B * w.H * w.N} of the workload's rows), {dt:.1f} s",
         "seconds": dt,
+        "extrapolated_full_seconds": dt * rows_total / done,
+        "extrapolated": "per-row time of the sample times all B*H*N query rows (labelled extrapolated, not run)",
         "host_cpus": len(os.sched_getaffinity(0)),
+        "cpu_model": cpu_model(),
+        "blas_threads": int(threads),
     }
 
 
@@ -168,13 +241,15 @@ def main():
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    wall0 = time.perf_counter()
-    start.record()
-    for i in range(args.steps):
-        step(events[i])
-    stop.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+    with SmiSampler() as smi:
+        wall0 = time.perf_counter()
+        start.record()
+        for i in range(args.steps):
+            step(events[i])
+        stop.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+    step_ms = [e[0].elapsed_time(e[4]) for e in events]
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
 
@@ -213,6 +288,12 @@ def main():
         else:
             per_kernel[n]["gbs"] = wk / (kern_ms[n] * 1e-3) / 1e9
 
+    smi_summary = smi.summary()
+    clock = None
+    if smi_summary:
+        # peak at the clock the chip actually held: 256 CU x 4096 flop/clk x sclk
+        peak_at_sclk = 256 * 4096 * smi_summary["sclk_mhz_median"] * 1e6 / 1e12
+        clock = dict(smi_summary, peak_tflops_at_sclk=peak_at_sclk, pct_of_peak_at_sclk=100.0 * value / peak_at_sclk)
     result = {
         "metric": "attention fwd+bwd TFLOP/s and % of bf16 MFMA peak at N=188,416, d=128",
         "value": value,
@@ -230,6 +311,9 @@ def main():
                    "grid": f"{w.grid[0]}x{w.grid[1]}", "seed": w.seed},
         "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "counted_tflop_per_step": flops["total"] / 1e12,
+        "step_ms_median": float(np.median(step_ms)),
+        "step_ms_min": float(np.min(step_ms)),
+        "clock": clock,
         "kernels": per_kernel,
         "wall_s_timed": wall,
         "roofline": roof,

@@ -294,7 +294,8 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 // One workgroup = NW waves = 32*NW query rows of one (b, h); each wave owns
 // 32 queries and keeps their Q and dO fragments (B operands), their LSE2 and
 // D and the dQ^T accumulator in registers. K and V stream through a ring of
-// four LDS slots in tiles of 32 keys. Per tile j the wave runs
+// six LDS slots in tiles of 32 keys (a barrier every second tile). Per tile j
+// the wave runs
 //   S^T = K_{j+1} Q^T and dP^T = V_{j+1} dO^T   (matrix cores)
 //     interleaved with P^T, dS^T of tile j      (vector units)
 //   dQ^T += K_j^T dS^T_j
@@ -314,20 +315,24 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   constexpr int NQ = KK;           // dQ ops per tile (2 contraction steps x NCB)
   constexpr int RPS = 16 / NS > 0 ? 16 / NS : 1;
   constexpr int TILE_BYTES = BN * D * 2;
-  constexpr int RING = 4;
+  constexpr int RING = 6;
   // One variable per ring slot (no wait for reads of one slot while the DMA
   // into another is in flight).
   __shared__ __attribute__((aligned(1024))) char kbuf0[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char kbuf1[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char kbuf2[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char kbuf3[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char kbuf4[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char kbuf5[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char vbuf0[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char vbuf1[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char vbuf2[TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char vbuf3[TILE_BYTES];
-  static_assert(RING == 4, "one variable per slot");
-  char* const kbuf[RING] = {kbuf0, kbuf1, kbuf2, kbuf3};
-  char* const vbuf[RING] = {vbuf0, vbuf1, vbuf2, vbuf3};
+  __shared__ __attribute__((aligned(1024))) char vbuf4[TILE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char vbuf5[TILE_BYTES];
+  static_assert(RING == 6, "one variable per slot");
+  char* const kbuf[RING] = {kbuf0, kbuf1, kbuf2, kbuf3, kbuf4, kbuf5};
+  char* const vbuf[RING] = {vbuf0, vbuf1, vbuf2, vbuf3, vbuf4, vbuf5};
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;
@@ -367,9 +372,9 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   for (int cb = 0; cb < NCB; ++cb) dqacc[cb] = zero16();
 
   const int n_kt = (N + BN - 1) / BN;
-  // prologue: tiles 0 .. RING-2 requested (tiles past the end read as zeros), scores of tile 0
+  // prologue: tiles 0 .. 3 requested (tiles past the end read as zeros), scores of tile 0
 #pragma unroll
-  for (int t = 0; t < RING - 1; ++t) {
+  for (int t = 0; t < 4; ++t) {
     dma.issue(rk, t * BN, kbuf[t]);
     dma.issue(rv, t * BN, vbuf[t]);
   }
@@ -384,54 +389,68 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   }
 
   // Stage j with SL = j % RING known at compile time: P, dS of tile j (from
-  // s, dp) and dQ of tile j (slot SL); scores of tile j+1 (slot SL+1) into
-  // sn, dpn; tile j+RING-1 requested into the slot of tile j-1.
+  // cur) and dQ of tile j (slot SL); scores of tile j+1 (slot SL+1) into nxt;
+  // tile j+4 requested into the slot of tile j-2. A barrier follows every
+  // second stage only: between two barriers the waves read three tiles
+  // (j .. j+2 of the first stage) while three more are in flight, hence six
+  // slots. The barrier after stage j waits for the requests of stage j-1 (for
+  // tile j+3, read from stage j+2 on) and leaves those of stage j in flight.
   auto stage = [&](auto slot_tag, auto has_next, f32x16 (&cur)[2], f32x16 (&nxt)[2], int j) {
     constexpr int SL = decltype(slot_tag)::value;
-    constexpr int NX = (SL + 1) % RING, RF = (SL + RING - 1) % RING;
+    constexpr int NX = (SL + 1) % RING, RF = (SL + 4) % RING;
     constexpr bool NEXT = decltype(has_next)::value;
-    if constexpr (NEXT) {
-      dma.issue(rk, (j + RING - 1) * BN, kbuf[RF]);
-      dma.issue(rv, (j + RING - 1) * BN, vbuf[RF]);
-    }
+    const char* ks = kbuf[SL];
     bf16x8 dsb[2];
-    auto valu = [&](int u) {
-#pragma unroll
-      for (int rr = 0; rr < RPS; ++rr) {
-        const int r = u * RPS + rr;
-        if (r < 16) {
-          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(cur[0][r], c, -l2));
-          float g = p * (cur[1][r] - dval);
-          pin(g);
-          cur[1][r] = g;
-          if ((r & 7) == 7) dsb[r >> 3] = acc_to_operand(cur[1], r >> 3);
-        }
-      }
+    // P^T and dS^T of accumulator row r of tile j
+    auto row = [&](int r) {
+      float p = __builtin_amdgcn_exp2f(__builtin_fmaf(cur[0][r], c, -l2));
+      float g = p * (cur[1][r] - dval);
+      pin(g);
+      cur[1][r] = g;
+      if ((r & 7) == 7) dsb[r >> 3] = acc_to_operand(cur[1], r >> 3);
     };
     if constexpr (NEXT) {
+      // One stream of NS score ops (tile j+1) then NQ dQ ops (tile j), each
+      // operand read one op ahead; row r of the vector work rides on op
+      // r*W/16, so dS rows 8..15 are complete two ops before the dQ op that
+      // first reads them.
+      constexpr int NOPS = NS + NQ;
+      constexpr int W = NS + NCB - 1;
+      static_assert(7 * W / 16 <= NS - 2 && 15 * W / 16 <= NS + NCB - 2, "dS ready before its dQ op");
+      auto load_op = [&](int i) -> bf16x8 {
+        if (i < KK) return lds_frag_row(kbuf[NX], rf.off[i]);
+        if (i < NS) return lds_frag_row(vbuf[NX], rf.off[i - KK]);
+        const int t = i - NS;
+        return tf.load(ks, 16 * (t / NCB), t % NCB);
+      };
       bf16x8 aq[2];
-      aq[0] = lds_frag_row(kbuf[NX], rf.off[0]);
+      aq[0] = load_op(0);
       sched_fence();
-#pragma unroll
-      for (int i = 0; i < NS; ++i) {
-        if (i + 1 < NS) {
-          const int n = i + 1;
-          aq[n & 1] = lds_frag_row(n < KK ? kbuf[NX] : vbuf[NX], rf.off[n % KK]);
+      static_for<0, NOPS>([&](auto IC) __attribute__((always_inline)) {
+        constexpr int i = decltype(IC)::value;
+        if constexpr (i + 1 < NOPS) aq[(i + 1) & 1] = load_op(i + 1);
+        if constexpr (i < NS) {
+          if constexpr (i % KK == 0) nxt[i / KK] = zero16();
+          nxt[i / KK] = mfma32(aq[i & 1], i < KK ? qf[i] : gf[i - KK], nxt[i / KK]);
+        } else {
+          constexpr int t = i - NS;
+          dqacc[t % NCB] = mfma32(aq[i & 1], dsb[t / NCB], dqacc[t % NCB]);
         }
-        if (i % KK == 0) nxt[i / KK] = zero16();
-        nxt[i / KK] = mfma32(aq[i & 1], i < KK ? qf[i] : gf[i - KK], nxt[i / KK]);
-        valu(i);
+        if constexpr (i == 1) dma.issue(rk, (j + 4) * BN, kbuf[RF]);
+        if constexpr (i == 3) dma.issue(rv, (j + 4) * BN, vbuf[RF]);
+        static_for<0, 16>([&](auto RC) __attribute__((always_inline)) {
+          constexpr int r = decltype(RC)::value;
+          if constexpr (r * W / 16 == i) row(r);
+        });
         sched_fence();
+      });
+      if constexpr ((SL & 1) == 1) {
+        wait_vmem_leave<2 * decltype(dma)::PER_WAVE>();
+        barrier_lds();
       }
-#pragma unroll
-      for (int i = NS; i < 16 / RPS; ++i) valu(i);
     } else {
 #pragma unroll
-      for (int i = 0; i < 16 / RPS; ++i) valu(i);
-    }
-    // dQ^T += K^T dS^T, K^T fragments read one op ahead
-    {
-      const char* ks = kbuf[SL];
+      for (int r = 0; r < 16; ++r) row(r);
       bf16x8 aq[2];
       aq[0] = tf.load(ks, 0, 0);
       sched_fence();
@@ -442,17 +461,14 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
         sched_fence();
       }
     }
-    if constexpr (NEXT) {
-      // tile j+2 must have landed; tile j+3 may still be in flight
-      wait_vmem_leave<2 * decltype(dma)::PER_WAVE>();
-      __syncthreads();
-    }
   };
 
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
   using S2 = std::integral_constant<int, 2>;
   using S3 = std::integral_constant<int, 3>;
+  using S4 = std::integral_constant<int, 4>;
+  using S5 = std::integral_constant<int, 5>;
   using Y = std::true_type;
   using F = std::false_type;
   // The tile count is rounded up to a multiple of the ring depth: the extra
@@ -465,11 +481,16 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
     stage(S1{}, Y{}, sb, sa, j + 1);
     stage(S2{}, Y{}, sa, sb, j + 2);
     stage(S3{}, Y{}, sb, sa, j + 3);
+    stage(S4{}, Y{}, sa, sb, j + 4);
+    stage(S5{}, Y{}, sb, sa, j + 5);
   }
   stage(S0{}, Y{}, sa, sb, j);
   stage(S1{}, Y{}, sb, sa, j + 1);
   stage(S2{}, Y{}, sa, sb, j + 2);
-  stage(S3{}, F{}, sb, sa, j + 3);
+  stage(S3{}, Y{}, sb, sa, j + 3);
+  stage(S4{}, Y{}, sa, sb, j + 4);
+  stage(S5{}, F{}, sb, sa, j + 5);
+  wait_vmem();  // requests past the last tile must land before this LDS is reassigned
 
   if (qrow < N) {
     float* row = dq + head_off + (size_t)qrow * D;

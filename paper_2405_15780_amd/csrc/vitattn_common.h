@@ -279,6 +279,18 @@ __device__ __forceinline__ void wait_vmem_leave() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CNT) : "memory");
 }
 
+// Workgroup barrier for LDS ring pipelines. The caller first waits for its
+// own LDS DMA requests that other waves will read (wait_vmem_leave); this
+// waits for the wave's own LDS reads and writes, then barriers. Unlike
+// __syncthreads() it does not wait for every outstanding vector-memory
+// access, so DMA requests for later tiles stay in flight across it; the
+// empty asm statements keep the compiler from moving memory accesses across.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Full scheduling fence: nothing moves across it. Used to pin an explicit
 // software pipeline (each step: one matrix-core op, the LDS read of an
 // operand needed a few steps later, a slice of unrelated vector work);
