@@ -22,4 +22,5 @@ from .attention import (  # noqa: F401
     row_statistics,
     key_rows,
 )
+from .segments import merge, segment_backward  # noqa: F401
 from . import naive  # noqa: F401
