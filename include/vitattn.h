@@ -110,6 +110,69 @@ int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout
                    int B, int H, int N, int d, float scale, const void* workspace, size_t workspace_bytes,
                    void* stream);
 
+/*
+ * Attention over one segment of the keys, and the merge of such partial
+ * results. Sequence parallelism over contiguous segments (Long Sequence
+ * Segmentation, paper Sec. I and II "Sequence Parallel": each GPU computes a
+ * partial self-attention for its segment) hands one GPU its queries and the
+ * keys of one segment at a time. Softmax over a union of key sets factors
+ * over the sets:
+ *
+ *     LSE_i = log sum_s exp(LSE_s,i),   O_i = sum_s exp(LSE_s,i - LSE_i) O_s,i
+ *
+ * and the backward pass of one segment, given the merged O and LSE, yields
+ * that segment's complete dK and dV rows and its share of dQ.
+ */
+
+/*
+ * Forward pass of Nq queries over Nk keys (vitattn_fwd is the case
+ * Nq = Nk = N; same algorithm, conventions and validation).
+ *   q        : bf16 [B][H][Nq][d];  k, v: bf16 [B][H][Nk][d].
+ *   o        : fp32 [B][H][Nq][d], written; lse: fp32 [B][H][Nq], written.
+ *   Nq, Nk   : each >= 1 and within the limits N obeys for vitattn_fwd.
+ */
+int vitattn_fwd_kv(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int Nq, int Nk,
+                   int d, float scale, void* stream);
+
+/* flags of vitattn_bwd_kv */
+#define VITATTN_BWD_ACCUMULATE_DQ 1 /* dq += this segment's share instead of dq = it */
+
+/*
+ * Backward pass of Nq queries over Nk keys (vitattn_bwd is the case
+ * Nq = Nk = N, flags = 0).
+ *   q, dout  : bf16 [B][H][Nq][d];  k, v: bf16 [B][H][Nk][d].
+ *   o, lse   : fp32 [B][H][Nq][d] and [B][H][Nq]: the output and LSE of the
+ *              attention the gradient flows through. For one key segment of a
+ *              larger key set pass the MERGED o and lse of all keys: then
+ *              dk, dv (fp32 [B][H][Nk][d], written) are exact for this
+ *              segment's keys and dq (fp32 [B][H][Nq][d]) is its share.
+ *   flags    : 0, or VITATTN_BWD_ACCUMULATE_DQ to add the share to dq (sum
+ *              the segments of one key set by calling once per segment on
+ *              one stream with dq zeroed first; the order of the sum is the
+ *              order of the calls). Other bits: VITATTN_E_INVAL.
+ *   workspace: at least vitattn_bwd_workspace_bytes(B, H, Nq, d) bytes.
+ */
+int vitattn_bwd_kv(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
+                   float* dq, float* dk, float* dv, int B, int H, int Nq, int Nk, int d, float scale, int flags,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* largest number of partial results vitattn_merge accepts */
+#define VITATTN_MERGE_MAX_PARTS 65536
+
+/*
+ * Merge n_parts partial attention results over disjoint key segments into
+ * the attention over all of them (the formula above).
+ *   o_parts  : fp32 [n_parts][B][H][N][d], read; lse_parts: fp32
+ *              [n_parts][B][H][N], read (each partial as written by
+ *              vitattn_fwd_kv for its segment).
+ *   o, lse   : fp32 [B][H][N][d] and [B][H][N], written; they must not alias
+ *              the partials.
+ *   n_parts  : 1 .. VITATTN_MERGE_MAX_PARTS, else VITATTN_E_INVAL.
+ * A NaN partial LSE makes the merged row NaN. Bound by HBM bandwidth.
+ */
+int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, float* o, float* lse, int B, int H,
+                  int N, int d, void* stream);
+
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* vitattn_status_str(int status);
 

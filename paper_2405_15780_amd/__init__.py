@@ -8,6 +8,7 @@ fallback path.
 """
 from .binding import (  # noqa: F401
     LIB_PATH,
+    VITATTN_BWD_ACCUMULATE_DQ,
     VitattnError,
     bwd,
     bwd_dkdv,
@@ -15,6 +16,7 @@ from .binding import (  # noqa: F401
     bwd_rowdot,
     fwd,
     library,
+    merge,
     status_str,
     version,
     workspace_bytes,

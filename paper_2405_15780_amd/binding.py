@@ -26,6 +26,9 @@ _SIGNATURES = {
     "vitattn_bwd_rowdot": (c_int, [c_void_p] * 3 + [c_int] * 4 + [c_void_p, c_size_t, c_void_p]),
     "vitattn_bwd_dkdv": (c_int, [c_void_p] * 7 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
     "vitattn_bwd_dq": (c_int, [c_void_p] * 6 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
+    "vitattn_fwd_kv": (c_int, [c_void_p] * 5 + [c_int] * 5 + [c_float, c_void_p]),
+    "vitattn_bwd_kv": (c_int, [c_void_p] * 9 + [c_int] * 5 + [c_float, c_int, c_void_p, c_size_t, c_void_p]),
+    "vitattn_merge": (c_int, [c_void_p] * 2 + [c_int] + [c_void_p] * 2 + [c_int] * 4 + [c_void_p]),
     "vitattn_status_str": (ctypes.c_char_p, [c_int]),
     "vitattn_version": (ctypes.c_char_p, []),
 }
@@ -92,21 +95,36 @@ def _default_scale(d, scale):
     return 1.0 / math.sqrt(d) if scale is None else float(scale)
 
 
+VITATTN_BWD_ACCUMULATE_DQ = 1
+
+
+def _kv_shapes(q, k, v):
+    B, H, Nq, d = q.shape
+    if k.shape != v.shape or k.shape[:2] != q.shape[:2] or k.shape[3] != d:
+        raise ValueError("k and v must be [B, H, Nk, d] with the B, H and d of q")
+    return B, H, Nq, k.shape[2], d
+
+
 def fwd(q, k, v, scale=None, out=None):
-    """O (fp32 [B,H,N,d]) and LSE (fp32 [B,H,N]) of softmax(scale Q K^T) V."""
+    """O (fp32 [B,H,Nq,d]) and LSE (fp32 [B,H,Nq]) of softmax(scale Q K^T) V;
+    k and v may hold a different number of rows Nk (one key segment)."""
     torch = _torch()
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _as_input(t, n)
-    B, H, N, d = q.shape
-    if k.shape != q.shape or v.shape != q.shape:
-        raise ValueError("q, k and v must have the same shape")
+    B, H, Nq, Nk, d = _kv_shapes(q, k, v)
     if out is None:
-        o = torch.empty((B, H, N, d), dtype=torch.float32, device=q.device)
-        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+        o = torch.empty((B, H, Nq, d), dtype=torch.float32, device=q.device)
+        lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
     else:
         o, lse = out
-    _check(library().vitattn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), B, H, N, d,
-                                 _default_scale(d, scale), _stream_ptr(q)))
+    lib = library()
+    if Nq == Nk:
+        st = lib.vitattn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), B, H, Nq, d,
+                             _default_scale(d, scale), _stream_ptr(q))
+    else:
+        st = lib.vitattn_fwd_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), B, H, Nq, Nk,
+                                d, _default_scale(d, scale), _stream_ptr(q))
+    _check(st)
     return o, lse
 
 
@@ -119,21 +137,54 @@ def _workspace(q, workspace):
     return workspace, workspace.numel() * workspace.element_size()
 
 
-def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None):
-    """dQ, dK, dV (fp32 [B,H,N,d]) for the upstream gradient dout (bf16)."""
+def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None, accumulate_dq=False):
+    """dQ (fp32 [B,H,Nq,d]), dK, dV (fp32 [B,H,Nk,d]) for the upstream gradient
+    dout (bf16). For one key segment pass the merged o and lse of all keys;
+    accumulate_dq adds this segment's share to out[0] instead of overwriting."""
     torch = _torch()
     for t, n in ((q, "q"), (k, "k"), (v, "v"), (dout, "dout")):
         _as_input(t, n)
-    B, H, N, d = q.shape
+    B, H, Nq, Nk, d = _kv_shapes(q, k, v)
     ws, ws_bytes = _workspace(q, workspace)
     if out is None:
-        dq, dk, dv = (torch.empty((B, H, N, d), dtype=torch.float32, device=q.device) for _ in range(3))
+        if accumulate_dq:
+            raise ValueError("accumulate_dq needs out=(dq, dk, dv) holding the running dq")
+        dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=q.device)
+        dk, dv = (torch.empty((B, H, Nk, d), dtype=torch.float32, device=q.device) for _ in range(2))
     else:
         dq, dk, dv = out
-    _check(library().vitattn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(),
-                                 lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, N, d,
-                                 _default_scale(d, scale), ws.data_ptr(), ws_bytes, _stream_ptr(q)))
+    lib = library()
+    if Nq == Nk and not accumulate_dq:
+        st = lib.vitattn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(), lse.data_ptr(),
+                             dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, Nq, d, _default_scale(d, scale),
+                             ws.data_ptr(), ws_bytes, _stream_ptr(q))
+    else:
+        st = lib.vitattn_bwd_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(),
+                                lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, Nq, Nk, d,
+                                _default_scale(d, scale), VITATTN_BWD_ACCUMULATE_DQ if accumulate_dq else 0,
+                                ws.data_ptr(), ws_bytes, _stream_ptr(q))
+    _check(st)
     return dq, dk, dv
+
+
+def merge(o_parts, lse_parts, out=None):
+    """Merge partial results over disjoint key segments: o_parts fp32
+    [P,B,H,N,d], lse_parts fp32 [P,B,H,N] -> (o [B,H,N,d], lse [B,H,N])."""
+    torch = _torch()
+    if not (o_parts.is_cuda and o_parts.dtype == torch.float32 and o_parts.dim() == 5 and o_parts.is_contiguous()):
+        raise TypeError("o_parts must be a contiguous 5-D float32 CUDA tensor [P, B, H, N, d]")
+    P, B, H, N, d = o_parts.shape
+    if not (lse_parts.is_cuda and lse_parts.dtype == torch.float32 and lse_parts.is_contiguous()
+            and tuple(lse_parts.shape) == (P, B, H, N)):
+        raise TypeError("lse_parts must be a contiguous float32 CUDA tensor [P, B, H, N]")
+    if out is None:
+        o = torch.empty((B, H, N, d), dtype=torch.float32, device=o_parts.device)
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=o_parts.device)
+    else:
+        o, lse = out
+    _check(library().vitattn_merge(o_parts.data_ptr(), lse_parts.data_ptr(), P, o.data_ptr(), lse.data_ptr(), B, H,
+                                   N, d, _stream_ptr(o_parts)))
+    return o, lse
 
 
 def bwd_rowdot(o, dout, lse, workspace):

@@ -10,7 +10,7 @@
 #include "../../include/vitattn.h"
 #include "vitattn_launch.h"
 
-#define VITATTN_VERSION "0.1.0"
+#define VITATTN_VERSION "0.2.0"
 
 namespace {
 
@@ -28,6 +28,12 @@ int check_sizes(int B, int H, int N, int d) {
 }
 
 bool scale_ok(float s) { return isfinite(s) && s > 0.f; }
+
+// key rows obey the same limits as query rows
+int check_sizes_kv(int B, int H, int Nq, int Nk, int d) {
+  const int st = check_sizes(B, H, Nq, d);
+  return st != VITATTN_OK ? st : check_sizes(B, H, Nk, d);
+}
 
 }  // namespace
 
@@ -61,8 +67,13 @@ size_t vitattn_bwd_workspace_bytes(int B, int H, int N, int d) {
 
 int vitattn_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int N, int d,
                 float scale, void* stream) {
+  return vitattn_fwd_kv(q, k, v, o, lse, B, H, N, N, d, scale, stream);
+}
+
+int vitattn_fwd_kv(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int Nq, int Nk,
+                   int d, float scale, void* stream) {
   try {
-    int st = check_sizes(B, H, N, d);
+    int st = check_sizes_kv(B, H, Nq, Nk, d);
     if (st != VITATTN_OK) return st;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
       return VITATTN_E_INVAL;
@@ -74,7 +85,8 @@ int vitattn_fwd(const void* q, const void* k, const void* v, float* o, float* ls
     a.o = o;
     a.lse = lse;
     a.BH = B * H;
-    a.N = N;
+    a.Nq = Nq;
+    a.Nk = Nk;
     a.d = d;
     a.scale = scale;
     a.stream = static_cast<hipStream_t>(stream);
@@ -92,8 +104,8 @@ static int check_workspace(const void* ws, size_t bytes, int B, int H, int N, in
 }
 
 static vitattn::BwdArgs bwd_args(const void* q, const void* k, const void* v, const float* o, const void* dout,
-                                 const float* lse, float* dq, float* dk, float* dv, int B, int H, int N, int d,
-                                 float scale, const void* workspace, void* stream) {
+                                 const float* lse, float* dq, float* dk, float* dv, int B, int H, int Nq, int Nk,
+                                 int d, float scale, bool accumulate_dq, const void* workspace, void* stream) {
   vitattn::BwdArgs a;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -105,11 +117,13 @@ static vitattn::BwdArgs bwd_args(const void* q, const void* k, const void* v, co
   a.dk = dk;
   a.dv = dv;
   a.drow = static_cast<float*>(const_cast<void*>(workspace));
-  a.lse2 = a.drow + vitattn::bwd_region_floats((long long)B * H * N);
+  a.lse2 = a.drow + vitattn::bwd_region_floats((long long)B * H * Nq);
   a.BH = B * H;
-  a.N = N;
+  a.Nq = Nq;
+  a.Nk = Nk;
   a.d = d;
   a.scale = scale;
+  a.accumulate_dq = accumulate_dq;
   a.stream = static_cast<hipStream_t>(stream);
   return a;
 }
@@ -117,17 +131,49 @@ static vitattn::BwdArgs bwd_args(const void* q, const void* k, const void* v, co
 int vitattn_bwd(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
                 float* dq, float* dk, float* dv, int B, int H, int N, int d, float scale, void* workspace,
                 size_t workspace_bytes, void* stream) {
+  return vitattn_bwd_kv(q, k, v, o, dout, lse, dq, dk, dv, B, H, N, N, d, scale, 0, workspace, workspace_bytes,
+                        stream);
+}
+
+int vitattn_bwd_kv(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
+                   float* dq, float* dk, float* dv, int B, int H, int Nq, int Nk, int d, float scale, int flags,
+                   void* workspace, size_t workspace_bytes, void* stream) {
   try {
-    int st = check_sizes(B, H, N, d);
+    int st = check_sizes_kv(B, H, Nq, Nk, d);
     if (st != VITATTN_OK) return st;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(lse) ||
         !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
       return VITATTN_E_INVAL;
     if (!scale_ok(scale)) return VITATTN_E_INVAL;
-    st = check_workspace(workspace, workspace_bytes, B, H, N, d);
+    if ((flags & ~VITATTN_BWD_ACCUMULATE_DQ) != 0) return VITATTN_E_INVAL;
+    st = check_workspace(workspace, workspace_bytes, B, H, Nq, d);
     if (st != VITATTN_OK) return st;
-    const vitattn::BwdArgs a = bwd_args(q, k, v, o, dout, lse, dq, dk, dv, B, H, N, d, scale, workspace, stream);
+    const vitattn::BwdArgs a = bwd_args(q, k, v, o, dout, lse, dq, dk, dv, B, H, Nq, Nk, d, scale,
+                                        (flags & VITATTN_BWD_ACCUMULATE_DQ) != 0, workspace, stream);
     return vitattn::launch_bwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, float* o, float* lse, int B, int H,
+                  int N, int d, void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (n_parts < 1 || n_parts > VITATTN_MERGE_MAX_PARTS) return VITATTN_E_INVAL;
+    if (!aligned16(o_parts) || !aligned16(lse_parts) || !aligned16(o) || !aligned16(lse)) return VITATTN_E_INVAL;
+    vitattn::MergeArgs a;
+    a.o_parts = o_parts;
+    a.lse_parts = lse_parts;
+    a.o = o;
+    a.lse = lse;
+    a.P = n_parts;
+    a.BH = B * H;
+    a.N = N;
+    a.d = d;
+    a.stream = static_cast<hipStream_t>(stream);
+    return vitattn::launch_merge(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
   } catch (...) {
     return VITATTN_E_INTERNAL;
   }
@@ -142,7 +188,7 @@ int vitattn_bwd_rowdot(const float* o, const void* dout, const float* lse, int B
     st = check_workspace(workspace, workspace_bytes, B, H, N, d);
     if (st != VITATTN_OK) return st;
     const vitattn::BwdArgs a = bwd_args(nullptr, nullptr, nullptr, o, dout, lse, nullptr, nullptr, nullptr, B, H, N,
-                                        d, 1.f, workspace, stream);
+                                        N, d, 1.f, false, workspace, stream);
     return vitattn::launch_bwd_rowdot(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
   } catch (...) {
     return VITATTN_E_INTERNAL;
@@ -162,7 +208,7 @@ int vitattn_bwd_dkdv(const void* q, const void* k, const void* v, const void* do
     st = check_workspace(workspace, workspace_bytes, B, H, N, d);
     if (st != VITATTN_OK) return st;
     const vitattn::BwdArgs a =
-        bwd_args(q, k, v, nullptr, dout, lse, nullptr, dk, dv, B, H, N, d, scale, workspace, stream);
+        bwd_args(q, k, v, nullptr, dout, lse, nullptr, dk, dv, B, H, N, N, d, scale, false, workspace, stream);
     return vitattn::launch_bwd_dkdv(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
   } catch (...) {
     return VITATTN_E_INTERNAL;
@@ -181,7 +227,7 @@ int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout
     st = check_workspace(workspace, workspace_bytes, B, H, N, d);
     if (st != VITATTN_OK) return st;
     const vitattn::BwdArgs a =
-        bwd_args(q, k, v, nullptr, dout, lse, dq, nullptr, nullptr, B, H, N, d, scale, workspace, stream);
+        bwd_args(q, k, v, nullptr, dout, lse, dq, nullptr, nullptr, B, H, N, N, d, scale, false, workspace, stream);
     return vitattn::launch_bwd_dq(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
   } catch (...) {
     return VITATTN_E_INTERNAL;

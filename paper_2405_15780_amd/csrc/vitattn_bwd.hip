@@ -93,7 +93,7 @@ template <int D>
 __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
-    float* __restrict__ dk, float* __restrict__ dv, int N, int n_ktiles, int total, float c, float scale) {
+    float* __restrict__ dk, float* __restrict__ dv, int Nq, int Nk, int n_ktiles, int total, float c, float scale) {
   constexpr int KK = D / 16, NCB = D / 32;
   constexpr int PH = KK;           // ops per phase
   constexpr int NOPS = 4 * PH;     // ops per tile
@@ -127,16 +127,17 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   const int kb = wave & 3;
   const bool role_p = wave < 4;
 
-  const size_t head_off = (size_t)bh * N * D;
-  const unsigned head_bytes = (unsigned)N * (2 * D);
-  const rsrc_t rq = make_rsrc(q + head_off, head_bytes);
-  const rsrc_t rg = make_rsrc(dout + head_off, head_bytes);
-  const rsrc_t rd = make_rsrc(drow + (size_t)bh * N, (unsigned)N * 4);
-  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * N, (unsigned)N * 4);
+  // queries, dO and the row statistics have Nq rows per (b, h); K, V, dK, dV have Nk
+  const size_t head_off = (size_t)bh * Nq * D;
+  const size_t kv_off = (size_t)bh * Nk * D;
+  const rsrc_t rq = make_rsrc(q + head_off, (unsigned)Nq * (2 * D));
+  const rsrc_t rg = make_rsrc(dout + head_off, (unsigned)Nq * (2 * D));
+  const rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)Nq * 4);
+  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)Nq * 4);
 
   // held fragments (B operands, columns = this block's keys): K for role P, V for role dS
   const int key = kt * kDkvBK + kb * 32 + (lane & 31);
-  const rsrc_t rh = make_rsrc((role_p ? k : v) + head_off, head_bytes);
+  const rsrc_t rh = make_rsrc((role_p ? k : v) + kv_off, (unsigned)Nk * (2 * D));
   bf16x8 hf[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) hf[kk] = as_bf16x8(buffer_load16(rh, key * (2 * D) + 32 * kk + 16 * h));
@@ -249,7 +250,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // Iteration t: role P on tile t (slot t % 3), role dS on tile t-1, tile t+1
   // requested into slot (t+1) % 3. Rounding the tile count to 1 mod 3 lets
   // iterations 1 .. n_pad-1 run in groups of three with fixed slots.
-  const int n_qt = (N + kDkvBQ - 1) / kDkvBQ;
+  const int n_qt = (Nq + kDkvBQ - 1) / kDkvBQ;
   const int n_pad = n_qt + (3 + 1 - n_qt % 3) % 3;
   auto iteration = [&](auto slot_p, auto slot_next, auto slot_ds, int t, bool do_p, bool do_ds) {
     // tile t+1 past the end: zero rows, never read
@@ -277,8 +278,8 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   if (!role_p) run_tile(RoleDs{}, S0{}, [] {});
   (void)DMA_PER_TILE;
 
-  if (key < N) {
-    float* out = (role_p ? dv : dk) + head_off + (size_t)key * D;
+  if (key < Nk) {
+    float* out = (role_p ? dv : dk) + kv_off + (size_t)key * D;
     const float f = role_p ? 1.f : scale;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
@@ -307,7 +308,7 @@ template <int D, int NW>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
-    float* __restrict__ dq, int N, int n_qtiles, int total, float c, float scale) {
+    float* __restrict__ dq, int Nq, int Nk, int n_qtiles, int total, float c, float scale, int accumulate) {
   constexpr int BM = 32 * NW;
   constexpr int BN = 32;
   constexpr int KK = D / 16, NCB = D / 32;
@@ -340,12 +341,13 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
 
-  const size_t head_off = (size_t)bh * N * D;
-  const unsigned head_bytes = (unsigned)N * (2 * D);
-  const rsrc_t rq = make_rsrc(q + head_off, head_bytes);
-  const rsrc_t rg = make_rsrc(dout + head_off, head_bytes);
-  const rsrc_t rk = make_rsrc(k + head_off, head_bytes);
-  const rsrc_t rv = make_rsrc(v + head_off, head_bytes);
+  // queries, dO, dQ and the row statistics have Nq rows per (b, h); K and V have Nk
+  const size_t head_off = (size_t)bh * Nq * D;
+  const size_t kv_off = (size_t)bh * Nk * D;
+  const rsrc_t rq = make_rsrc(q + head_off, (unsigned)Nq * (2 * D));
+  const rsrc_t rg = make_rsrc(dout + head_off, (unsigned)Nq * (2 * D));
+  const rsrc_t rk = make_rsrc(k + kv_off, (unsigned)Nk * (2 * D));
+  const rsrc_t rv = make_rsrc(v + kv_off, (unsigned)Nk * (2 * D));
 
   const int qrow = qt * BM + wave * 32 + (lane & 31);
   bf16x8 qf[KK], gf[KK];
@@ -354,8 +356,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
     qf[kk] = as_bf16x8(buffer_load16(rq, qrow * (2 * D) + 32 * kk + 16 * h));
     gf[kk] = as_bf16x8(buffer_load16(rg, qrow * (2 * D) + 32 * kk + 16 * h));
   }
-  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * N, (unsigned)N * 4);
-  const rsrc_t rd = make_rsrc(drow + (size_t)bh * N, (unsigned)N * 4);
+  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)Nq * 4);
+  const rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)Nq * 4);
   // (the b32 buffer load returns the raw bits)
   const float l2 = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, qrow * 4, 0, 0));
   const float dval = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, qrow * 4, 0, 0));
@@ -371,7 +373,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) dqacc[cb] = zero16();
 
-  const int n_kt = (N + BN - 1) / BN;
+  const int n_kt = (Nk + BN - 1) / BN;
   // prologue: tiles 0 .. 3 requested (tiles past the end read as zeros), scores of tile 0
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
@@ -492,15 +494,21 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   stage(S5{}, F{}, sb, sa, j + 5);
   wait_vmem();  // requests past the last tile must land before this LDS is reassigned
 
-  if (qrow < N) {
+  if (qrow < Nq) {
     float* row = dq + head_off + (size_t)qrow * D;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
-        *reinterpret_cast<float4*>(row + 32 * cb + 8 * g + 4 * h) =
-            make_float4(dqacc[cb][4 * g] * scale, dqacc[cb][4 * g + 1] * scale, dqacc[cb][4 * g + 2] * scale,
-                        dqacc[cb][4 * g + 3] * scale);
+      for (int g = 0; g < 4; ++g) {
+        float4* dst = reinterpret_cast<float4*>(row + 32 * cb + 8 * g + 4 * h);
+        float4 val = make_float4(dqacc[cb][4 * g] * scale, dqacc[cb][4 * g + 1] * scale,
+                                 dqacc[cb][4 * g + 2] * scale, dqacc[cb][4 * g + 3] * scale);
+        if (accumulate) {  // this call's dQ is one key segment's share
+          const float4 prev = *dst;
+          val = make_float4(prev.x + val.x, prev.y + val.y, prev.z + val.z, prev.w + val.w);
+        }
+        *dst = val;
+      }
   }
 }
 
@@ -508,7 +516,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
 
 template <int D>
 static hipError_t rowdot_d(const BwdArgs& a) {
-  const long rows = (long)a.BH * a.N;
+  const long rows = (long)a.BH * a.Nq;
   constexpr int rows_per_block = 256 / (D / 8);
   hipLaunchKernelGGL(attn_bwd_rowdot_kernel<D>, dim3((unsigned)((rows + rows_per_block - 1) / rows_per_block)),
                      dim3(256), 0, a.stream, a.dout, a.o, a.lse, a.drow, a.lse2, rows);
@@ -517,10 +525,10 @@ static hipError_t rowdot_d(const BwdArgs& a) {
 
 template <int D>
 static hipError_t dkdv_d(const BwdArgs& a) {
-  const int n_kt = (a.N + kDkvBK - 1) / kDkvBK;
+  const int n_kt = (a.Nk + kDkvBK - 1) / kDkvBK;
   const int total = a.BH * n_kt;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(total), dim3(2 * kBwdThreads), 0, a.stream, a.q, a.k, a.v,
-                     a.dout, a.drow, a.lse2, a.dk, a.dv, a.N, n_kt, total, a.scale * kLog2e, a.scale);
+                     a.dout, a.drow, a.lse2, a.dk, a.dv, a.Nq, a.Nk, n_kt, total, a.scale * kLog2e, a.scale);
   return hipGetLastError();
 }
 
@@ -528,17 +536,18 @@ static hipError_t dkdv_d(const BwdArgs& a) {
   template __global__ void attn_bwd_dkdv_kernel<D>(                                                        \
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,            \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
-      float* __restrict__, int, int, int, float, float);
+      float* __restrict__, int, int, int, int, float, float);
 VITATTN_DKDV_INSTANTIATE(128)
 VITATTN_DKDV_INSTANTIATE(64)
 #undef VITATTN_DKDV_INSTANTIATE
 
 template <int D, int NW>
 static hipError_t dq_v(const BwdArgs& a) {
-  const int n_qt = (a.N + 32 * NW - 1) / (32 * NW);
+  const int n_qt = (a.Nq + 32 * NW - 1) / (32 * NW);
   const int total = a.BH * n_qt;
   hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v, a.dout,
-                     a.drow, a.lse2, a.dq, a.N, n_qt, total, a.scale * kLog2e, a.scale);
+                     a.drow, a.lse2, a.dq, a.Nq, a.Nk, n_qt, total, a.scale * kLog2e, a.scale,
+                     a.accumulate_dq ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -546,7 +555,7 @@ static hipError_t dq_v(const BwdArgs& a) {
   template __global__ void attn_bwd_dq_kernel<D, NW>(                                                      \
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,            \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
-      int, int, int, float, float);
+      int, int, int, int, float, float, int);
 VITATTN_DQ_INSTANTIATE(128, 4)
 VITATTN_DQ_INSTANTIATE(128, 8)
 VITATTN_DQ_INSTANTIATE(64, 4)

@@ -55,7 +55,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
                                                                  const uint16_t* __restrict__ k,
                                                                  const uint16_t* __restrict__ v,
                                                                  float* __restrict__ o, float* __restrict__ lse,
-                                                                 int N, int n_qtiles, int total, float c) {
+                                                                 int Nq, int Nk, int n_qtiles, int total, float c) {
   constexpr int BM = 32 * NW;  // query rows per workgroup
   constexpr int BN = 32 * KB;  // keys per tile
   constexpr int TILE_BYTES = BN * D * 2;
@@ -78,11 +78,12 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
 
-  const size_t head_off = (size_t)bh * N * D;
-  const unsigned head_bytes = (unsigned)N * (2 * D);
-  const rsrc_t rq = make_rsrc(q + head_off, head_bytes);
-  const rsrc_t rk = make_rsrc(k + head_off, head_bytes);
-  const rsrc_t rv = make_rsrc(v + head_off, head_bytes);
+  // queries (and O, LSE) have Nq rows per (b, h), keys and values Nk
+  const size_t head_off = (size_t)bh * Nq * D;
+  const size_t kv_off = (size_t)bh * Nk * D;
+  const rsrc_t rq = make_rsrc(q + head_off, (unsigned)Nq * (2 * D));
+  const rsrc_t rk = make_rsrc(k + kv_off, (unsigned)Nk * (2 * D));
+  const rsrc_t rv = make_rsrc(v + kv_off, (unsigned)Nk * (2 * D));
 
   // Q fragments of this wave's 32 query rows (B operands of K Q^T)
   const int qrow = qt * BM + wave * 32 + (lane & 31);
@@ -103,7 +104,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   float m_run = -INFINITY;  // running max of scaled logits, log2 units
   float l_part = 0.f;       // this lane's share of the sum of the bf16 probabilities
 
-  const int n_kt = (N + BN - 1) / BN;
+  const int n_kt = (Nk + BN - 1) / BN;
   dma.issue(rk, 0, kbuf[0]);
   dma.issue(rv, 0, vbuf[0]);
   dma.issue(rk, BN, kbuf[1]);
@@ -114,12 +115,12 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   // keys past the end arrive as zeros; their scores become -inf
   auto mask_ragged = [&](f32x16 (&s)[KB], int tile) {
     const int key0 = tile * BN;
-    if (key0 + BN > N) {
+    if (key0 + BN > Nk) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (key0 + kb * 32 + acc_row(r, h) >= N) s[kb][r] = -INFINITY;
+          if (key0 + kb * 32 + acc_row(r, h) >= Nk) s[kb][r] = -INFINITY;
     }
   };
   // lane-local maximum of quarter q of a tile's scores
@@ -280,7 +281,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
 
   // epilogue: O = O^T / l (stored transposed back to [query][d]), LSE in nats.
   const float l = sum_halves(l_part);
-  if (qrow < N) {
+  if (qrow < Nq) {
     const float inv = 1.0f / l;
     float* orow = o + head_off + (size_t)qrow * D;
 #pragma unroll
@@ -291,18 +292,18 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
                                  oacc[cb][4 * g + 3] * inv);
         *reinterpret_cast<float4*>(orow + 32 * cb + 8 * g + 4 * h) = val;
       }
-    if (h == 0) lse[(size_t)bh * N + qrow] = (m_run + __log2f(l)) * kLn2;
+    if (h == 0) lse[(size_t)bh * Nq + qrow] = (m_run + __log2f(l)) * kLn2;
   }
 }
 
 template <int D, int KB, int NW, int MINW>
 static hipError_t launch_fwd_v(const FwdArgs& a) {
   constexpr int BM = 32 * NW;
-  const int n_qtiles = (a.N + BM - 1) / BM;
+  const int n_qtiles = (a.Nq + BM - 1) / BM;
   const int total = a.BH * n_qtiles;
   const float c = a.scale * kLog2e;
   hipLaunchKernelGGL((attn_fwd_kernel<D, KB, NW, MINW>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v,
-                     a.o, a.lse, a.N, n_qtiles, total, c);
+                     a.o, a.lse, a.Nq, a.Nk, n_qtiles, total, c);
   return hipGetLastError();
 }
 
@@ -316,7 +317,7 @@ static hipError_t launch_fwd_v(const FwdArgs& a) {
                                                             const uint16_t* __restrict__,               \
                                                             const uint16_t* __restrict__,               \
                                                             float* __restrict__, float* __restrict__, int, \
-                                                            int, int, float);
+                                                            int, int, int, float);
 VITATTN_FWD_VARIANTS(VITATTN_FWD_INSTANTIATE)
 #undef VITATTN_FWD_INSTANTIATE
 

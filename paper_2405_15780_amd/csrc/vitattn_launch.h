@@ -12,7 +12,7 @@ struct FwdArgs {
   const uint16_t* v;
   float* o;
   float* lse;
-  int BH, N, d;
+  int BH, Nq, Nk, d;  // query rows and key rows per (b, h)
   float scale;
   hipStream_t stream;
 };
@@ -27,10 +27,20 @@ struct BwdArgs {
   float* dq;
   float* dk;
   float* dv;
-  float* drow;  // workspace region 0: D = rowsum(dO o O), [BH][N]
-  float* lse2;  // workspace region 1: LSE * log2(e), [BH][N]
-  int BH, N, d;
+  float* drow;  // workspace region 0: D = rowsum(dO o O), [BH][Nq]
+  float* lse2;  // workspace region 1: LSE * log2(e), [BH][Nq]
+  int BH, Nq, Nk, d;  // query rows and key rows per (b, h)
   float scale;
+  bool accumulate_dq;  // dq += this call's dQ instead of dq = ...
+  hipStream_t stream;
+};
+
+struct MergeArgs {
+  const float* o_parts;    // [P][BH][N][d]
+  const float* lse_parts;  // [P][BH][N]
+  float* o;                // [BH][N][d]
+  float* lse;              // [BH][N]
+  int P, BH, N, d;
   hipStream_t stream;
 };
 
@@ -48,5 +58,6 @@ hipError_t launch_bwd_rowdot(const BwdArgs& a);
 hipError_t launch_bwd_dkdv(const BwdArgs& a);
 hipError_t launch_bwd_dq(const BwdArgs& a);
 hipError_t launch_bwd(const BwdArgs& a);
+hipError_t launch_merge(const MergeArgs& a);
 
 }  // namespace vitattn

@@ -30,14 +30,14 @@ def declared_functions():
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
     assert {"vitattn_fwd", "vitattn_bwd", "vitattn_bwd_workspace_bytes", "vitattn_status_str",
-            "vitattn_version"} <= set(names)
+            "vitattn_version", "vitattn_fwd_kv", "vitattn_bwd_kv", "vitattn_merge"} <= set(names)
     raw = ctypes.CDLL(va.LIB_PATH)
     for n in names:
         assert hasattr(raw, n), n
 
 
 def test_status_strings_and_version():
-    assert va.version() == "0.1.0"
+    assert va.version() == "0.2.0"
     for s in range(6):
         assert va.status_str(s).startswith("VITATTN")
     assert "unknown" in va.status_str(99)
@@ -148,6 +148,67 @@ def test_bwd_stages_validate():
                             None) == E_INVAL
     assert L.vitattn_bwd_dq(b.p(0), b.p(1), b.p(2), b.p(3), b.p(4), b.p(5), 1, 1, 8, 64, 0.1, b.p(7), 0,
                             None) == E_WS
+    assert b.untouched()
+
+
+def fwd_kv(b, B=1, H=1, Nq=8, Nk=5, d=64, scale=0.125, override=None):
+    ptrs = [b.p(i) for i in range(5)]
+    if override:
+        for i, val in override.items():
+            ptrs[i] = val
+    return lib().vitattn_fwd_kv(*ptrs, B, H, Nq, Nk, d, scale, None)
+
+
+@pytest.mark.parametrize("kw,expected", [
+    (dict(Nk=0), E_INVAL), (dict(Nq=0), E_INVAL), (dict(Nk=-1), E_INVAL), (dict(d=72), E_UNSUP),
+    (dict(Nk=8388352, d=128), E_INVAL), (dict(scale=float("nan")), E_INVAL),
+    (dict(override={1: None}), E_INVAL), (dict(override={2: 4100}), E_INVAL),
+])
+def test_fwd_kv_rejects_bad_arguments(kw, expected):
+    b = Bufs()
+    assert fwd_kv(b, **kw) == expected
+    assert b.untouched()
+
+
+def bwd_kv(b, B=1, H=1, Nq=8, Nk=5, d=64, scale=0.125, flags=0, ws_bytes=None, override=None):
+    ptrs = [b.p(i) for i in range(9)]
+    if override:
+        for i, val in override.items():
+            ptrs[i] = val
+    wsb = va.workspace_bytes(1, 1, max(Nq, 1), 64) if ws_bytes is None else ws_bytes
+    return lib().vitattn_bwd_kv(*ptrs, B, H, Nq, Nk, d, scale, flags, b.p(9), wsb, None)
+
+
+@pytest.mark.parametrize("kw,expected", [
+    (dict(Nk=0), E_INVAL), (dict(flags=2), E_INVAL), (dict(flags=-1), E_INVAL), (dict(d=160), E_UNSUP),
+    (dict(ws_bytes=1), E_WS), (dict(override={6: None}), E_INVAL), (dict(override={7: 4102}), E_INVAL),
+])
+def test_bwd_kv_rejects_bad_arguments(kw, expected):
+    b = Bufs()
+    assert bwd_kv(b, **kw) == expected
+    assert b.untouched()
+
+
+def test_bwd_kv_workspace_is_sized_by_query_rows():
+    b = Bufs(n=1 << 16)
+    # 200 query rows need more workspace than 8: too small for Nq = 200
+    assert bwd_kv(b, Nq=200, Nk=8, ws_bytes=va.workspace_bytes(1, 1, 8, 64)) == E_WS
+    assert b.untouched()
+
+
+@pytest.mark.parametrize("kw,expected", [
+    (dict(P=0), E_INVAL), (dict(P=-3), E_INVAL), (dict(P=65537), E_INVAL), (dict(N=0), E_INVAL),
+    (dict(d=96), E_UNSUP), (dict(override={0: None}), E_INVAL), (dict(override={3: 4104}), E_INVAL),
+])
+def test_merge_rejects_bad_arguments(kw, expected):
+    b = Bufs()
+    args = dict(P=2, B=1, H=1, N=8, d=64)
+    args.update({k: v for k, v in kw.items() if k != "override"})
+    ptrs = [b.p(i) for i in range(4)]
+    for i, val in kw.get("override", {}).items():
+        ptrs[i] = val
+    assert lib().vitattn_merge(ptrs[0], ptrs[1], args["P"], ptrs[2], ptrs[3], args["B"], args["H"], args["N"],
+                               args["d"], None) == expected
     assert b.untouched()
 
 
