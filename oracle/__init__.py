@@ -23,4 +23,5 @@ from .attention import (  # noqa: F401
     key_rows,
 )
 from .segments import merge, segment_backward  # noqa: F401
+from . import ulysses  # noqa: F401
 from . import naive  # noqa: F401
