@@ -173,6 +173,32 @@ int vitattn_bwd_kv(const void* q, const void* k, const void* v, const float* o, 
 int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, float* o, float* lse, int B, int H,
                   int N, int d, void* stream);
 
+/*
+ * Layouts around DeepSpeed-Ulysses' all-to-all (paper Sec. II "Sequence
+ * Parallel"; two all-to-alls per attention in each pass, Sec. V). Each of P
+ * ranks holds Nl tokens of all H heads (rank r: tokens r*Nl .. r*Nl+Nl-1);
+ * attention needs the whole sequence N = P*Nl of Hl = H/P heads. With
+ * rows of row_bytes bytes (one token of one head, e.g. d bf16 values):
+ *
+ *   pack       x    [B][Nl][H]       -> send [P][B][Hl][Nl]   send[p][b][j][i] = x[b][i][p*Hl+j]
+ *   (all-to-all: chunk p of rank r's send buffer becomes chunk r of rank p's receive buffer)
+ *   unpack     recv [P][B][Hl][Nl]   -> y    [B][Hl][P*Nl]    y[b][j][r*Nl+i] = recv[r][b][j][i]
+ *   pack_out   y    [B][Hl][P*Nl]    -> send [P][B][Hl][Nl]   (inverse of unpack)
+ *   unpack_out recv [P][B][Hl][Nl]   -> x    [B][Nl][H]       (inverse of pack)
+ *
+ * y is the contiguous [B][Hl][N][row] input (or output) of the attention
+ * entry points. The collective itself is not part of this library.
+ *   B, Nl, H, P: >= 1 with H divisible by P, P*B <= 65535, Nl*row_bytes/16 < 2^31.
+ *   row_bytes  : a multiple of 16, >= 16.
+ *   src, dst   : device pointers, 16-byte aligned, not overlapping
+ *                (src == dst is rejected; partial overlap is not detected).
+ * Pure copies, bound by HBM bandwidth. Returns a vitattn_status.
+ */
+int vitattn_ulysses_pack(const void* x, void* send, int B, int Nl, int H, int P, int row_bytes, void* stream);
+int vitattn_ulysses_unpack(const void* recv, void* y, int B, int Nl, int H, int P, int row_bytes, void* stream);
+int vitattn_ulysses_pack_out(const void* y, void* send, int B, int Nl, int H, int P, int row_bytes, void* stream);
+int vitattn_ulysses_unpack_out(const void* recv, void* x, int B, int Nl, int H, int P, int row_bytes, void* stream);
+
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* vitattn_status_str(int status);
 

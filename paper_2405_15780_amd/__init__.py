@@ -18,6 +18,10 @@ from .binding import (  # noqa: F401
     library,
     merge,
     status_str,
+    ulysses_pack,
+    ulysses_pack_out,
+    ulysses_unpack,
+    ulysses_unpack_out,
     version,
     workspace_bytes,
 )

@@ -29,6 +29,10 @@ _SIGNATURES = {
     "vitattn_fwd_kv": (c_int, [c_void_p] * 5 + [c_int] * 5 + [c_float, c_void_p]),
     "vitattn_bwd_kv": (c_int, [c_void_p] * 9 + [c_int] * 5 + [c_float, c_int, c_void_p, c_size_t, c_void_p]),
     "vitattn_merge": (c_int, [c_void_p] * 2 + [c_int] + [c_void_p] * 2 + [c_int] * 4 + [c_void_p]),
+    "vitattn_ulysses_pack": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
+    "vitattn_ulysses_unpack": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
+    "vitattn_ulysses_pack_out": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
+    "vitattn_ulysses_unpack_out": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
     "vitattn_status_str": (ctypes.c_char_p, [c_int]),
     "vitattn_version": (ctypes.c_char_p, []),
 }
@@ -206,3 +210,58 @@ def bwd_dq(q, k, v, dout, lse, dq, workspace, scale=None):
     _check(library().vitattn_bwd_dq(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
                                     dq.data_ptr(), B, H, N, d, _default_scale(d, scale), workspace.data_ptr(),
                                     workspace.numel() * workspace.element_size(), _stream_ptr(q)))
+
+
+def _rows(t, lead, name):
+    """(leading dims, row shape, row_bytes) of a contiguous CUDA tensor whose
+    first `lead` dims index rows."""
+    if not (t.is_cuda and t.is_contiguous() and t.dim() > lead):
+        raise TypeError(f"{name} must be a contiguous CUDA tensor with more than {lead} dims")
+    row_shape = tuple(t.shape[lead:])
+    row_bytes = t.element_size()
+    for n in row_shape:
+        row_bytes *= n
+    return tuple(t.shape[:lead]), row_shape, row_bytes
+
+
+def _ulysses(status, dst):
+    _check(status)
+    return dst
+
+
+def ulysses_pack(x, P):
+    """x [B, Nl, H, *row] -> send [P, B, H/P, Nl, *row] (head group p in chunk p)."""
+    torch = _torch()
+    (B, Nl, H), row, rb = _rows(x, 3, "x")
+    send = torch.empty((P, B, H // P, Nl) + row, dtype=x.dtype, device=x.device)
+    return _ulysses(library().vitattn_ulysses_pack(x.data_ptr(), send.data_ptr(), B, Nl, H, P, rb, _stream_ptr(x)),
+                    send)
+
+
+def ulysses_unpack(recv):
+    """recv [P, B, Hl, Nl, *row] (chunk r from rank r) -> y [B, Hl, P*Nl, *row]."""
+    torch = _torch()
+    (P, B, Hl, Nl), row, rb = _rows(recv, 4, "recv")
+    y = torch.empty((B, Hl, P * Nl) + row, dtype=recv.dtype, device=recv.device)
+    return _ulysses(library().vitattn_ulysses_unpack(recv.data_ptr(), y.data_ptr(), B, Nl, Hl * P, P, rb,
+                                                     _stream_ptr(recv)), y)
+
+
+def ulysses_pack_out(y, P):
+    """y [B, Hl, P*Nl, *row] -> send [P, B, Hl, Nl, *row] (the inverse of unpack)."""
+    torch = _torch()
+    (B, Hl, N), row, rb = _rows(y, 3, "y")
+    if N % P != 0:
+        raise ValueError("the sequence length must be divisible by P")
+    send = torch.empty((P, B, Hl, N // P) + row, dtype=y.dtype, device=y.device)
+    return _ulysses(library().vitattn_ulysses_pack_out(y.data_ptr(), send.data_ptr(), B, N // P, Hl * P, P, rb,
+                                                       _stream_ptr(y)), send)
+
+
+def ulysses_unpack_out(recv):
+    """recv [P, B, Hl, Nl, *row] -> x [B, Nl, P*Hl, *row] (the inverse of pack)."""
+    torch = _torch()
+    (P, B, Hl, Nl), row, rb = _rows(recv, 4, "recv")
+    x = torch.empty((B, Nl, P * Hl) + row, dtype=recv.dtype, device=recv.device)
+    return _ulysses(library().vitattn_ulysses_unpack_out(recv.data_ptr(), x.data_ptr(), B, Nl, Hl * P, P, rb,
+                                                         _stream_ptr(recv)), x)

@@ -234,4 +234,45 @@ int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout
   }
 }
 
+static int ulysses(const void* src, void* dst, int B, int Nl, int H, int P, int row_bytes, int mode, void* stream) {
+  try {
+    if (B < 1 || Nl < 1 || H < 1 || P < 1 || H % P != 0) return VITATTN_E_INVAL;
+    if (row_bytes < 16 || row_bytes % 16 != 0) return VITATTN_E_INVAL;
+    if (!aligned16(src) || !aligned16(dst) || src == dst) return VITATTN_E_INVAL;
+    // grid limits: P*B and H/P index grid dimensions, Nl*row_bytes/16 a 32-bit thread index
+    if ((long long)P * B > 65535 || (long long)Nl * (row_bytes / 16) > 0x7fffffffLL) return VITATTN_E_INVAL;
+    if ((double)B * Nl * H * row_bytes > 9.0e18) return VITATTN_E_INVAL;
+    vitattn::UlyssesArgs a;
+    a.src = src;
+    a.dst = dst;
+    a.B = B;
+    a.Nl = Nl;
+    a.H = H;
+    a.P = P;
+    a.row_bytes = row_bytes;
+    a.mode = mode;
+    a.stream = static_cast<hipStream_t>(stream);
+    return vitattn::launch_ulysses(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+int vitattn_ulysses_pack(const void* x, void* send, int B, int Nl, int H, int P, int row_bytes, void* stream) {
+  return ulysses(x, send, B, Nl, H, P, row_bytes, vitattn::kUlyssesPack, stream);
+}
+
+int vitattn_ulysses_unpack(const void* recv, void* y, int B, int Nl, int H, int P, int row_bytes, void* stream) {
+  return ulysses(recv, y, B, Nl, H, P, row_bytes, vitattn::kUlyssesUnpack, stream);
+}
+
+int vitattn_ulysses_pack_out(const void* y, void* send, int B, int Nl, int H, int P, int row_bytes, void* stream) {
+  return ulysses(y, send, B, Nl, H, P, row_bytes, vitattn::kUlyssesPackOut, stream);
+}
+
+int vitattn_ulysses_unpack_out(const void* recv, void* x, int B, int Nl, int H, int P, int row_bytes,
+                               void* stream) {
+  return ulysses(recv, x, B, Nl, H, P, row_bytes, vitattn::kUlyssesUnpackOut, stream);
+}
+
 }  // extern "C"

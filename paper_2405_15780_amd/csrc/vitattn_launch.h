@@ -60,4 +60,14 @@ hipError_t launch_bwd_dq(const BwdArgs& a);
 hipError_t launch_bwd(const BwdArgs& a);
 hipError_t launch_merge(const MergeArgs& a);
 
+// Ulysses layout copies (see vitattn_ulysses.hip for the row orders)
+enum { kUlyssesPack = 0, kUlyssesUnpack = 1, kUlyssesPackOut = 2, kUlyssesUnpackOut = 3 };
+struct UlyssesArgs {
+  const void* src;
+  void* dst;
+  int B, Nl, H, P, row_bytes, mode;
+  hipStream_t stream;
+};
+hipError_t launch_ulysses(const UlyssesArgs& a);
+
 }  // namespace vitattn

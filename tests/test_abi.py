@@ -212,6 +212,22 @@ def test_merge_rejects_bad_arguments(kw, expected):
     assert b.untouched()
 
 
+@pytest.mark.parametrize("name", ["vitattn_ulysses_pack", "vitattn_ulysses_unpack", "vitattn_ulysses_pack_out",
+                                  "vitattn_ulysses_unpack_out"])
+@pytest.mark.parametrize("kw", [dict(H=6, P=4), dict(P=0), dict(B=0), dict(Nl=0), dict(row_bytes=24),
+                                dict(row_bytes=0), dict(src=None), dict(dst=None), dict(src="dst"),
+                                dict(src=4100), dict(B=40000, P=2, H=2)])
+def test_ulysses_layouts_reject_bad_arguments(name, kw):
+    b = Bufs()
+    args = dict(src=b.p(0), dst=b.p(1), B=1, Nl=4, H=4, P=2, row_bytes=32)
+    args.update(kw)
+    if args["src"] == "dst":
+        args["src"] = args["dst"]
+    fn = getattr(lib(), name)
+    assert fn(args["src"], args["dst"], args["B"], args["Nl"], args["H"], args["P"], args["row_bytes"], None) == E_INVAL
+    assert b.untouched()
+
+
 def test_binding_helpers_reject_wrong_tensors():
     torch = pytest.importorskip("torch")
     x = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
