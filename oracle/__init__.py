@@ -24,4 +24,5 @@ from .attention import (  # noqa: F401
 )
 from .segments import merge, segment_backward  # noqa: F401
 from . import ulysses  # noqa: F401
+from . import aggregation  # noqa: F401
 from . import naive  # noqa: F401
