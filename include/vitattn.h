@@ -199,6 +199,38 @@ int vitattn_ulysses_unpack(const void* recv, void* y, int B, int Nl, int H, int 
 int vitattn_ulysses_pack_out(const void* y, void* send, int B, int Nl, int H, int P, int row_bytes, void* stream);
 int vitattn_ulysses_unpack_out(const void* recv, void* x, int B, int Nl, int H, int P, int row_bytes, void* stream);
 
+/*
+ * Channel aggregation by attention with a learnable query: the Agg-Ch-ViT
+ * layer (paper Sec. II "Patch Embedding and Sequence Length") folds the C
+ * channel tokens of each patch into one token. For M patch positions (batch
+ * x patches) and H heads, one query q_h per head, shared by every patch,
+ * attends over that patch's projected channel keys and values:
+ *
+ *   s_c = scale q_h . k_mhc,  lse_mh = log sum_c exp(s_c),  o_mh = sum_c exp(s_c - lse_mh) v_mhc
+ *
+ * and the backward pass (dq sums over every patch, as q is shared):
+ *
+ *   ds_c = p_c (do_mh . v_mhc - do_mh . o_mh),  dk_mhc = scale ds_c q_h,
+ *   dv_mhc = p_c do_mh,  dq_h = scale sum_m sum_c ds_c k_mhc.
+ *
+ * Layouts (row-major): q bf16 [H][d]; k, v bf16 [M][H][C][d]; o fp32
+ * [M][H][d]; lse fp32 [M][H]; dout bf16 [M][H][d]; dq fp32 [H][d]; dk, dv
+ * fp32 [M][H][C][d]. M, H, C >= 1 (any C; the paper's case is C = 92);
+ * d in {64, 128}; scale finite and > 0. Bound by HBM bandwidth. dq is
+ * reduced in a fixed order (no atomics): results are bitwise reproducible.
+ */
+int vitattn_agg_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int M, int H, int C, int d,
+                    float scale, void* stream);
+
+/* Workspace bytes of vitattn_agg_bwd (per-block dq partials); 0 for invalid sizes. */
+size_t vitattn_agg_bwd_workspace_bytes(int M, int H, int C, int d);
+
+/* o and lse are vitattn_agg_fwd's outputs for the same q, k, v; workspace is
+ * overwritten and must not alias any other argument. */
+int vitattn_agg_bwd(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
+                    float* dq, float* dk, float* dv, int M, int H, int C, int d, float scale, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* vitattn_status_str(int status);
 

@@ -10,6 +10,8 @@ from .binding import (  # noqa: F401
     LIB_PATH,
     VITATTN_BWD_ACCUMULATE_DQ,
     VitattnError,
+    agg_bwd,
+    agg_fwd,
     bwd,
     bwd_dkdv,
     bwd_dq,

@@ -8,7 +8,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB_PATH = os.path.join(HERE, "libvitattn.so")
-SOURCES = ["vitattn_api.hip", "vitattn_fwd.hip", "vitattn_bwd.hip", "vitattn_merge.hip", "vitattn_ulysses.hip"]
+SOURCES = ["vitattn_api.hip", "vitattn_fwd.hip", "vitattn_bwd.hip", "vitattn_merge.hip", "vitattn_ulysses.hip", "vitattn_agg.hip"]
 ARCH = "gfx950"
 
 HIP_FLAGS = [

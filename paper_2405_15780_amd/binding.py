@@ -29,6 +29,9 @@ _SIGNATURES = {
     "vitattn_fwd_kv": (c_int, [c_void_p] * 5 + [c_int] * 5 + [c_float, c_void_p]),
     "vitattn_bwd_kv": (c_int, [c_void_p] * 9 + [c_int] * 5 + [c_float, c_int, c_void_p, c_size_t, c_void_p]),
     "vitattn_merge": (c_int, [c_void_p] * 2 + [c_int] + [c_void_p] * 2 + [c_int] * 4 + [c_void_p]),
+    "vitattn_agg_fwd": (c_int, [c_void_p] * 5 + [c_int] * 4 + [c_float, c_void_p]),
+    "vitattn_agg_bwd_workspace_bytes": (c_size_t, [c_int] * 4),
+    "vitattn_agg_bwd": (c_int, [c_void_p] * 9 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
     "vitattn_ulysses_pack": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
     "vitattn_ulysses_unpack": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
     "vitattn_ulysses_pack_out": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
@@ -265,3 +268,45 @@ def ulysses_unpack_out(recv):
     x = torch.empty((B, Nl, P * Hl) + row, dtype=recv.dtype, device=recv.device)
     return _ulysses(library().vitattn_ulysses_unpack_out(recv.data_ptr(), x.data_ptr(), B, Nl, Hl * P, P, rb,
                                                          _stream_ptr(recv)), x)
+
+
+def _agg_shapes(q, k, v):
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        if not (t.is_cuda and t.dtype == _torch().bfloat16 and t.is_contiguous()):
+            raise TypeError(f"{n} must be a contiguous bfloat16 CUDA tensor")
+    if q.dim() != 2 or k.dim() != 4 or k.shape != v.shape or k.shape[1] != q.shape[0] or k.shape[3] != q.shape[1]:
+        raise ValueError("q must be [H, d] and k, v [M, H, C, d]")
+    M, H, C, d = k.shape
+    return M, H, C, d
+
+
+def agg_fwd(q, k, v, scale=None):
+    """Channel aggregation: o (fp32 [M,H,d]) and lse (fp32 [M,H]) of one shared
+    query per head (q [H,d]) over each patch's C channel keys (k, v [M,H,C,d])."""
+    torch = _torch()
+    M, H, C, d = _agg_shapes(q, k, v)
+    o = torch.empty((M, H, d), dtype=torch.float32, device=k.device)
+    lse = torch.empty((M, H), dtype=torch.float32, device=k.device)
+    _check(library().vitattn_agg_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), M, H, C,
+                                     d, _default_scale(d, scale), _stream_ptr(k)))
+    return o, lse
+
+
+def agg_bwd(q, k, v, o, lse, dout, scale=None):
+    """Gradients of the channel aggregation: dq (fp32 [H,d], summed over all
+    patches), dk and dv (fp32 [M,H,C,d])."""
+    torch = _torch()
+    M, H, C, d = _agg_shapes(q, k, v)
+    if not (dout.is_cuda and dout.dtype == torch.bfloat16 and dout.is_contiguous()
+            and tuple(dout.shape) == (M, H, d)):
+        raise TypeError("dout must be a contiguous bfloat16 CUDA tensor [M, H, d]")
+    lib = library()
+    wsb = int(lib.vitattn_agg_bwd_workspace_bytes(M, H, C, d))
+    ws = torch.empty(max(wsb, 4) // 4, dtype=torch.float32, device=k.device)
+    dq = torch.empty((H, d), dtype=torch.float32, device=k.device)
+    dk = torch.empty((M, H, C, d), dtype=torch.float32, device=k.device)
+    dv = torch.empty_like(dk)
+    _check(lib.vitattn_agg_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(),
+                               lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), M, H, C, d,
+                               _default_scale(d, scale), ws.data_ptr(), ws.numel() * 4, _stream_ptr(k)))
+    return dq, dk, dv

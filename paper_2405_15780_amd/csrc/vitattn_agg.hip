@@ -1,0 +1,257 @@
+// Channel aggregation by attention with a learnable query (the Agg-Ch-ViT
+// layer, paper Sec. II "Patch Embedding and Sequence Length"): per patch
+// position m and head h, one query q_h shared by every patch attends over
+// the C channel tokens of that patch:
+//
+//   s_c = scale q_h . k_mhc,  LSE = log sum_c exp(s_c),  o_mh = sum_c exp(s_c - LSE) v_mhc
+//
+// and the backward pass (dq_h sums over all patches, as q is shared):
+//
+//   dp_c = do . v_c,  D = do . o,  ds_c = p_c (dp_c - D),
+//   dk_c = scale ds_c q_h,  dv_c = p_c do,  dq_h = scale sum_m sum_c ds_c k_c
+//
+// Many tiny attentions, bound by HBM bandwidth: one wave per (m, h). Scores
+// and their dot products are lane-per-key (a lane reads its whole key row);
+// the weighted sums over keys are lane-per-column (each V, K, dK, dV row is
+// one coalesced 64-lane access) with the key's probability broadcast by
+// readlane. dq is reduced without atomics: each block sums a fixed range of
+// patches into a partial in the workspace, then one pass adds the partials
+// in order, so results are bitwise reproducible.
+#include <math.h>
+
+#include "vitattn_common.h"
+#include "vitattn_launch.h"
+
+namespace vitattn {
+
+namespace {
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// dot product of a full d-element bf16 row (this lane's key) with the fp32
+// vector x in LDS (the same address for every lane: a broadcast read)
+template <int D>
+__device__ __forceinline__ float row_dot(const uint16_t* row, const float* x) {
+  const uint4* r = reinterpret_cast<const uint4*>(row);
+  const float4* xv = reinterpret_cast<const float4*>(x);
+  float acc = 0.f;
+#pragma unroll 4
+  for (int t = 0; t < D / 8; ++t) {
+    const uint4 w = r[t];
+    const float4 a = xv[2 * t], b = xv[2 * t + 1];
+    acc = fmaf(bf16_lo(w.x), a.x, acc);
+    acc = fmaf(bf16_hi(w.x), a.y, acc);
+    acc = fmaf(bf16_lo(w.y), a.z, acc);
+    acc = fmaf(bf16_hi(w.y), a.w, acc);
+    acc = fmaf(bf16_lo(w.z), b.x, acc);
+    acc = fmaf(bf16_hi(w.z), b.y, acc);
+    acc = fmaf(bf16_lo(w.w), b.z, acc);
+    acc = fmaf(bf16_hi(w.w), b.w, acc);
+  }
+  return acc;
+}
+
+// this lane's E = D/64 consecutive columns of a bf16 row, widened
+template <int D>
+__device__ __forceinline__ void row_cols(const uint16_t* row, int lane, float (&out)[D / 64]) {
+  if constexpr (D == 128) {
+    const uint32_t w = reinterpret_cast<const uint32_t*>(row)[lane];
+    out[0] = bf16_lo(w);
+    out[1] = bf16_hi(w);
+  } else {
+    out[0] = __uint_as_float((uint32_t)row[lane] << 16);
+  }
+}
+
+// a bf16 d-vector widened into this wave's LDS slot (each lane its columns)
+template <int D>
+__device__ __forceinline__ void stage_vec(const uint16_t* src, float* dst, int lane) {
+  float x[D / 64];
+  row_cols<D>(src, lane, x);
+#pragma unroll
+  for (int e = 0; e < D / 64; ++e) dst[lane * (D / 64) + e] = x[e];
+}
+
+}  // namespace
+
+template <int D>
+__global__ __launch_bounds__(256) void attn_agg_fwd_kernel(const uint16_t* __restrict__ q,
+                                                           const uint16_t* __restrict__ k,
+                                                           const uint16_t* __restrict__ v, float* __restrict__ o,
+                                                           float* __restrict__ lse, int MH, int H, int C, float c2) {
+  constexpr int E = D / 64;  // columns per lane
+  __shared__ __attribute__((aligned(16))) float qs[4][D];
+  const int wave = threadIdx.x >> 6;
+  const int inst = blockIdx.x * 4 + wave;
+  if (inst >= MH) return;  // whole waves exit together; no block barrier follows
+  const int lane = threadIdx.x & 63;
+  const int h = inst % H;
+  float* qx = qs[wave];
+  stage_vec<D>(q + (size_t)h * D, qx, lane);  // a wave's own LDS writes precede its reads
+  const uint16_t* kb = k + (size_t)inst * C * D;
+  const uint16_t* vb = v + (size_t)inst * C * D;
+
+  float m_run = -INFINITY, l = 0.f;  // log2 units
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  for (int c0 = 0; c0 < C; c0 += 64) {
+    const int c = c0 + lane;
+    const float s = c < C ? row_dot<D>(kb + (size_t)c * D, qx) * c2 : -INFINITY;
+    const float m_new = fmaxf(m_run, wave_max(s));
+    const float alpha = exp2f(m_run - m_new);
+    const float p = c < C ? exp2f(s - m_new) : 0.f;
+    l = l * alpha + wave_sum(p);
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] *= alpha;
+    const int n = min(64, C - c0);
+    for (int j = 0; j < n; ++j) {
+      const float pj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p), j));
+      float vc[E];
+      row_cols<D>(vb + (size_t)(c0 + j) * D, lane, vc);
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] = fmaf(pj, vc[e], acc[e]);
+    }
+    m_run = m_new;
+  }
+  const float inv = 1.f / l;
+#pragma unroll
+  for (int e = 0; e < E; ++e) o[(size_t)inst * D + lane * E + e] = acc[e] * inv;
+  if (lane == 0) lse[inst] = (m_run + log2f(l)) * kLn2;
+}
+
+// Block (chunk, h): waves take patches m = chunk*per + w, + 4, ... below
+// (chunk+1)*per and write dk, dv; the block's share of dq_h goes to
+// partial[chunk][h][:].
+template <int D>
+__global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    const float* __restrict__ o, const uint16_t* __restrict__ dout, const float* __restrict__ lse,
+    float* __restrict__ dk, float* __restrict__ dv, float* __restrict__ partial, int M, int H, int C, int per,
+    float c2, float scale) {
+  constexpr int E = D / 64;
+  __shared__ __attribute__((aligned(16))) float red[4][D];
+  __shared__ __attribute__((aligned(16))) float qs[D];
+  __shared__ __attribute__((aligned(16))) float gs[4][D];
+  const int chunk = blockIdx.x, h = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (wave == 0) stage_vec<D>(q + (size_t)h * D, qs, lane);
+  __syncthreads();
+  const float* qx = qs;
+  float* gx = gs[wave];
+  float dq[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) dq[e] = 0.f;
+  const int m_end = min(M, (chunk + 1) * per);
+  for (int m = chunk * per + wave; m < m_end; m += 4) {
+    const size_t inst = (size_t)m * H + h;
+    const uint16_t* kb = k + inst * C * D;
+    const uint16_t* vb = v + inst * C * D;
+    float* dkb = dk + inst * C * D;
+    float* dvb = dv + inst * C * D;
+    // dO of this instance: in the wave's LDS slot (for dp) and its own columns
+    stage_vec<D>(dout + inst * D, gx, lane);
+    float g[E], oc[E];
+    row_cols<D>(dout + inst * D, lane, g);
+#pragma unroll
+    for (int e = 0; e < E; ++e) oc[e] = o[inst * D + lane * E + e];
+    float dpart = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) dpart = fmaf(g[e], oc[e], dpart);
+    const float Dm = wave_sum(dpart);
+    const float l2 = lse[inst] * kLog2e;
+    for (int c0 = 0; c0 < C; c0 += 64) {
+      const int c = c0 + lane;
+      float p = 0.f, ds = 0.f;
+      if (c < C) {
+        p = exp2f(row_dot<D>(kb + (size_t)c * D, qx) * c2 - l2);
+        ds = p * (row_dot<D>(vb + (size_t)c * D, gx) - Dm);
+      }
+      const int n = min(64, C - c0);
+      for (int j = 0; j < n; ++j) {
+        const float pj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p), j));
+        const float dsj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ds), j));
+        const size_t row = (size_t)(c0 + j) * D;
+        float kc[E];
+        row_cols<D>(kb + row, lane, kc);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          dkb[row + lane * E + e] = scale * dsj * qx[lane * E + e];
+          dvb[row + lane * E + e] = pj * g[e];
+          dq[e] = fmaf(dsj, kc[e], dq[e]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) red[wave][lane * E + e] = dq[e];
+  __syncthreads();
+  if (threadIdx.x < D) {
+    const float s = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
+    partial[((size_t)chunk * H + h) * D + threadIdx.x] = s;
+  }
+}
+
+// dq[h][e] = scale * sum over chunks, in chunk order
+__global__ __launch_bounds__(256) void attn_agg_dq_kernel(const float* __restrict__ partial, float* __restrict__ dq,
+                                                          int chunks, int HD, float scale) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= HD) return;
+  float s = 0.f;
+  for (int c = 0; c < chunks; ++c) s += partial[(size_t)c * HD + t];
+  dq[t] = scale * s;
+}
+
+#define VITATTN_AGG_INSTANTIATE(D)                                                                             \
+  template __global__ void attn_agg_fwd_kernel<D>(const uint16_t* __restrict__, const uint16_t* __restrict__, \
+                                                  const uint16_t* __restrict__, float* __restrict__,          \
+                                                  float* __restrict__, int, int, int, float);                 \
+  template __global__ void attn_agg_bwd_kernel<D>(                                                             \
+      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
+      const float* __restrict__, const uint16_t* __restrict__, const float* __restrict__, float* __restrict__, \
+      float* __restrict__, float* __restrict__, int, int, int, int, float, float);
+VITATTN_AGG_INSTANTIATE(64)
+VITATTN_AGG_INSTANTIATE(128)
+#undef VITATTN_AGG_INSTANTIATE
+
+int agg_chunks(int M) { return M < kAggMaxChunks ? M : kAggMaxChunks; }
+
+template <int D>
+static hipError_t agg_fwd_d(const AggArgs& a) {
+  const int MH = a.M * a.H;
+  hipLaunchKernelGGL(attn_agg_fwd_kernel<D>, dim3((unsigned)((MH + 3) / 4)), dim3(256), 0, a.stream, a.q, a.k, a.v,
+                     a.o_out, a.lse_out, MH, a.H, a.C, a.scale * kLog2e);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t agg_bwd_d(const AggArgs& a) {
+  const int chunks = agg_chunks(a.M);
+  const int per = (a.M + chunks - 1) / chunks;
+  hipLaunchKernelGGL(attn_agg_bwd_kernel<D>, dim3((unsigned)chunks, (unsigned)a.H), dim3(256), 0, a.stream, a.q, a.k,
+                     a.v, a.o, a.dout, a.lse, a.dk, a.dv, a.partial, a.M, a.H, a.C, per, a.scale * kLog2e, a.scale);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int HD = a.H * D;
+  hipLaunchKernelGGL(attn_agg_dq_kernel, dim3((unsigned)((HD + 255) / 256)), dim3(256), 0, a.stream, a.partial, a.dq,
+                     chunks, HD, a.scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_agg_fwd(const AggArgs& a) { return a.d == 128 ? agg_fwd_d<128>(a) : agg_fwd_d<64>(a); }
+hipError_t launch_agg_bwd(const AggArgs& a) { return a.d == 128 ? agg_bwd_d<128>(a) : agg_bwd_d<64>(a); }
+
+}  // namespace vitattn

@@ -275,4 +275,76 @@ int vitattn_ulysses_unpack_out(const void* recv, void* x, int B, int Nl, int H, 
   return ulysses(recv, x, B, Nl, H, P, row_bytes, vitattn::kUlyssesUnpackOut, stream);
 }
 
+static int check_agg(int M, int H, int C, int d, float scale) {
+  if (M < 1 || H < 1 || C < 1) return VITATTN_E_INVAL;
+  if (d != 64 && d != 128) return VITATTN_E_UNSUPPORTED;
+  if ((long long)M * H > 0x7fffffffLL || (long long)H * d > 0x7fffffffLL) return VITATTN_E_INVAL;
+  if ((double)M * H * C * d > 4.0e18) return VITATTN_E_INVAL;
+  return scale_ok(scale) ? VITATTN_OK : VITATTN_E_INVAL;
+}
+
+size_t vitattn_agg_bwd_workspace_bytes(int M, int H, int C, int d) {
+  if (check_agg(M, H, C, d, 1.f) != VITATTN_OK) return 0;
+  return (size_t)vitattn::agg_chunks(M) * H * d * sizeof(float);
+}
+
+int vitattn_agg_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int M, int H, int C, int d,
+                    float scale, void* stream) {
+  try {
+    const int st = check_agg(M, H, C, d, scale);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse)) return VITATTN_E_INVAL;
+    vitattn::AggArgs a = {};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.o_out = o;
+    a.lse_out = lse;
+    a.M = M;
+    a.H = H;
+    a.C = C;
+    a.d = d;
+    a.scale = scale;
+    a.stream = static_cast<hipStream_t>(stream);
+    return vitattn::launch_agg_fwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+int vitattn_agg_bwd(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
+                    float* dq, float* dk, float* dv, int M, int H, int C, int d, float scale, void* workspace,
+                    size_t workspace_bytes, void* stream) {
+  try {
+    int st = check_agg(M, H, C, d, scale);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(lse) ||
+        !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+      return VITATTN_E_INVAL;
+    if (workspace == nullptr || !aligned16(workspace) ||
+        workspace_bytes < vitattn_agg_bwd_workspace_bytes(M, H, C, d))
+      return VITATTN_E_WORKSPACE;
+    vitattn::AggArgs a = {};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.o = o;
+    a.dout = static_cast<const uint16_t*>(dout);
+    a.lse = lse;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.partial = static_cast<float*>(workspace);
+    a.M = M;
+    a.H = H;
+    a.C = C;
+    a.d = d;
+    a.scale = scale;
+    a.stream = static_cast<hipStream_t>(stream);
+    return vitattn::launch_agg_bwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
 }  // extern "C"

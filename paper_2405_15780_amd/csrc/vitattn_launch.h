@@ -70,4 +70,28 @@ struct UlyssesArgs {
 };
 hipError_t launch_ulysses(const UlyssesArgs& a);
 
+// Channel aggregation (attention of one learnable query per head over the C
+// channel tokens of each of M patches); see vitattn_agg.hip.
+constexpr int kAggMaxChunks = 1024;  // blocks along M in the backward pass (dq partials)
+struct AggArgs {
+  const uint16_t* q;     // [H][d]
+  const uint16_t* k;     // [M][H][C][d]
+  const uint16_t* v;     // [M][H][C][d]
+  const float* o;        // [M][H][d]      (backward input)
+  const uint16_t* dout;  // [M][H][d]
+  float* o_out;          // forward output
+  const float* lse;      // [M][H]         (backward input)
+  float* lse_out;        // forward output
+  float* dq;             // [H][d]
+  float* dk;             // [M][H][C][d]
+  float* dv;             // [M][H][C][d]
+  float* partial;        // workspace: [chunks][H][d]
+  int M, H, C, d;
+  float scale;
+  hipStream_t stream;
+};
+int agg_chunks(int M);
+hipError_t launch_agg_fwd(const AggArgs& a);
+hipError_t launch_agg_bwd(const AggArgs& a);
+
 }  // namespace vitattn

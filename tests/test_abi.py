@@ -228,6 +228,37 @@ def test_ulysses_layouts_reject_bad_arguments(name, kw):
     assert b.untouched()
 
 
+@pytest.mark.parametrize("kw,expected", [
+    (dict(M=0), E_INVAL), (dict(H=0), E_INVAL), (dict(C=0), E_INVAL), (dict(d=72), E_UNSUP),
+    (dict(scale=float("inf")), E_INVAL), (dict(scale=-1.0), E_INVAL), (dict(M=70000, H=70000), E_INVAL),
+    (dict(override={0: None}), E_INVAL), (dict(override={3: 4100}), E_INVAL),
+])
+def test_agg_fwd_rejects_bad_arguments(kw, expected):
+    b = Bufs()
+    a = dict(M=2, H=2, C=5, d=64, scale=0.125)
+    a.update({k: v for k, v in kw.items() if k != "override"})
+    ptrs = [b.p(i) for i in range(5)]
+    for i, val in kw.get("override", {}).items():
+        ptrs[i] = val
+    assert lib().vitattn_agg_fwd(*ptrs, a["M"], a["H"], a["C"], a["d"], a["scale"], None) == expected
+    assert b.untouched()
+
+
+def test_agg_bwd_validates_workspace_and_pointers():
+    b = Bufs()
+    L = lib()
+    wsb = L.vitattn_agg_bwd_workspace_bytes(3, 2, 5, 64)
+    assert wsb == 3 * 2 * 64 * 4
+    assert L.vitattn_agg_bwd_workspace_bytes(5000, 2, 5, 64) == 1024 * 2 * 64 * 4
+    assert L.vitattn_agg_bwd_workspace_bytes(0, 2, 5, 64) == 0
+    ptrs = [b.p(i) for i in range(9)]
+    assert L.vitattn_agg_bwd(*ptrs, 3, 2, 5, 64, 0.1, b.p(9), wsb - 4, None) == E_WS
+    assert L.vitattn_agg_bwd(*ptrs, 3, 2, 5, 64, 0.1, None, wsb, None) == E_WS
+    ptrs[6] = None
+    assert L.vitattn_agg_bwd(*ptrs, 3, 2, 5, 64, 0.1, b.p(9), wsb, None) == E_INVAL
+    assert b.untouched()
+
+
 def test_binding_helpers_reject_wrong_tensors():
     torch = pytest.importorskip("torch")
     x = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)

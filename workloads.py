@@ -143,3 +143,13 @@ def fingerprint(bits: np.ndarray) -> str:
     import hashlib
 
     return hashlib.sha256(np.ascontiguousarray(bits).tobytes()).hexdigest()[:16]
+
+
+def make_aggregation_inputs(M, H, C, d, seed, with_dout=True) -> dict:
+    """Seeded bf16 inputs of the channel aggregation: q (H, d), k and v
+    (M, H, C, d), and dout (M, H, d). Draw order q, k, v, dout."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    out = {"q": random_bf16(rng, (H, d)), "k": random_bf16(rng, (M, H, C, d)), "v": random_bf16(rng, (M, H, C, d))}
+    if with_dout:
+        out["dout"] = random_bf16(rng, (M, H, d))
+    return out
