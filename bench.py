@@ -42,36 +42,52 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 512 MiB device copy (to scale rocprofv3 FETCH_SIZE/WRITE_SIZE)")
+    p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg"], default="attention",
+                   help="which kernel family to time (default: the attention forward+backward hot path)")
     return p.parse_args()
 
 
 COPY_BYTES = 512 * 1024 * 1024
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_N188416_d128.json")
+ROW_TRAFFIC = {r: os.path.join(ROOT, "profiles", f"hbm_traffic_{r}.json") for r in ("merge", "ulysses", "agg")}
 
 
-def kernel_sources_digest():
-    """Hash of the HIP sources, to tell whether stored counter readings still
-    describe the kernels being timed."""
+KERNEL_FILES = {
+    "attention": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
+    "merge": ("vitattn_merge.hip",),
+    "ulysses": ("vitattn_ulysses.hip",),
+    "agg": ("vitattn_agg.hip",),
+}
+
+
+def kernel_sources_digest(row="attention"):
+    """Hash of the HIP sources that define one kernel family (plus the shared
+    headers), to tell whether stored counter readings still describe the
+    kernels being timed."""
     import hashlib
 
     csrc = os.path.join(ROOT, "paper_2405_15780_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(csrc)):
+    for name in sorted(KERNEL_FILES[row] + ("vitattn_common.h", "vitattn_launch.h")):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
 
 
-def stored_traffic(kernel, config_name):
+def stored_traffic(kernel, config_name, row="attention"):
     """HBM bytes per launch of `kernel` from the committed counter summary,
     or None if it is missing or was taken on different kernel sources."""
+    path = TRAFFIC_FILE if row == "attention" else ROW_TRAFFIC[row]
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("sources") != kernel_sources_digest() or rec.get("workload") != config_name:
+    if rec.get("sources") != kernel_sources_digest(row) or rec.get("workload") != config_name:
         return None
+    roof = rec.get("roofline")
+    if roof is not None and roof.get("kernel") == kernel:
+        return roof.get("hbm_bytes")
     k = rec.get("kernels", {}).get(kernel)
     return None if k is None else k.get("hbm_bytes_per_launch")
 
@@ -188,10 +204,155 @@ def cpu_baseline(w, x, budget_s):
     }
 
 
+ROW_DOC = {
+    "merge": "merge of 8 key-segment partials (O fp32, LSE) at B=1, H=2, N=188,416, d=128",
+    "ulysses": ("Ulysses layouts around both all-to-alls of one attention, 8 ranks, ViT-Base heads "
+                "(H=16, d=64) at N=188,416 (23,552 tokens per rank): pack + unpack of bf16 Q, K, V, "
+                "pack_out + unpack_out of fp32 O"),
+    "agg": ("channel aggregation fwd+bwd, Agg-Ch-ViT on ViT-Base heads: M=8,192 patch positions "
+            "(batch 4 x 2,048), H=16, C=92 channels, d=64"),
+}
+
+
+def time_events(fn, reps):
+    """Mean milliseconds of fn() over `reps` back-to-back calls (HIP events on
+    the current stream), after two warm-up calls."""
+    import torch
+
+    for _ in range(2):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def timed_cpu(fn, budget_s):
+    """Run fn() repeatedly for about budget_s seconds; returns (calls, seconds)."""
+    n, t0 = 0, time.perf_counter()
+    while n == 0 or time.perf_counter() - t0 < budget_s:
+        fn()
+        n += 1
+    return n, time.perf_counter() - t0
+
+
+def bench_row(args):
+    """Time one of the HBM-bound kernel families beside the attention (key-segment
+    merge, Ulysses layouts, channel aggregation) against the HBM roofline, with
+    the oracle timed beside it on a bounded sample. Algorithmic bytes are the
+    minimal ones: every input read once, every output written once."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2405_15780_amd as va
+    import workloads
+
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(0)
+    budget = min(args.cpu_seconds, 10.0)
+    per_kernel = {}
+    if args.row == "merge":
+        P, BH, N, d = 8, 2, 188416, 128
+        o_parts = torch.randn((P, 1, BH, N, d), device=dev, generator=g)
+        lse_parts = 3.0 * torch.randn((P, 1, BH, N), device=dev, generator=g)
+        outs = (torch.empty((1, BH, N, d), device=dev), torch.empty((1, BH, N), device=dev))
+        ms = time_events(lambda: va.merge(o_parts, lse_parts, out=outs), args.steps)
+        nbytes = (P + 1) * BH * N * (d + 1) * 4
+        dom, dom_ms, dom_bytes = "attn_merge_kernel", ms, nbytes
+        rows = 4096
+        op = o_parts[:, :, 0, :rows].double().cpu().numpy()
+        lp = lse_parts[:, :, 0, :rows].double().cpu().numpy()
+        cpu_fn, cpu_bytes = (lambda: oracle.merge(op, lp)), (P + 1) * rows * (d + 1) * 4
+        sample = f"fp64 merge of {rows} of the {BH * N} rows x {P} partials"
+    elif args.row == "ulysses":
+        P, B, Nl, H, d = 8, 1, 23552, 16, 64
+        Hl = H // P
+        ins = [torch.randn((B, Nl, H, d), device=dev, generator=g).to(torch.bfloat16) for _ in range(3)]
+        send = [torch.empty((P, B, Hl, Nl, d), device=dev, dtype=torch.bfloat16) for _ in range(3)]
+        att = [torch.empty((B, Hl, P * Nl, d), device=dev, dtype=torch.bfloat16) for _ in range(3)]
+        o_att = torch.randn((B, Hl, P * Nl, d), device=dev, generator=g)
+        o_send = torch.empty((P, B, Hl, Nl, d), device=dev)
+        o_back = torch.empty((B, Nl, H, d), device=dev)
+
+        def step():
+            # the all-to-all itself moves send -> recv between ranks; on one GPU
+            # recv is the send buffer
+            for x, s_, y in zip(ins, send, att):
+                va.ulysses_pack(x, P, out=s_)
+                va.ulysses_unpack(s_, out=y)
+            va.ulysses_pack_out(o_att, P, out=o_send)
+            va.ulysses_unpack_out(o_send, out=o_back)
+
+        ms = time_events(step, args.steps)
+        nbytes = 3 * 2 * 2 * B * Nl * H * d * 2 + 2 * 2 * B * Nl * H * d * 4
+        dom, dom_ms, dom_bytes = "ulysses_layout_kernel", ms, nbytes
+        xs = [x[:, :2048].view(torch.int16).cpu().numpy().view(np.uint16) for x in ins]
+        oo = o_send[:, :, :, :256].cpu().numpy()
+
+        def cpu_step():
+            for x in xs:
+                oracle.ulysses.unpack(oracle.ulysses.pack(x, P))
+            oracle.ulysses.unpack_out(oracle.ulysses.pack_out(oracle.ulysses.unpack(oo), P))
+
+        cpu_fn, cpu_bytes = cpu_step, 3 * 2 * 2 * xs[0].size * 2 + 3 * 2 * oo.size * 4
+        sample = f"numpy layouts of 2,048 of the {Nl} tokens per rank (Q, K, V) and 256 per rank of O"
+    else:
+        M, H, C, d = 8192, 16, 92, 64
+        q = torch.randn((H, d), device=dev, generator=g).to(torch.bfloat16)
+        k = torch.randn((M, H, C, d), device=dev, generator=g).to(torch.bfloat16)
+        v = torch.randn((M, H, C, d), device=dev, generator=g).to(torch.bfloat16)
+        dout = torch.randn((M, H, d), device=dev, generator=g).to(torch.bfloat16)
+        o, lse = va.agg_fwd(q, k, v)
+        kv = M * H * C * d
+        fwd_bytes = 2 * kv * 2 + M * H * (d + 1) * 4  # read K, V; write O, LSE
+        bwd_bytes = 2 * kv * 2 + M * H * (d * 4 + d * 2 + 4) + 2 * kv * 4  # + O, dO, LSE; write dK, dV
+        fwd_ms = time_events(lambda: va.agg_fwd(q, k, v), args.steps)
+        bwd_ms = time_events(lambda: va.agg_bwd(q, k, v, o, lse, dout), args.steps)
+        ms, nbytes = fwd_ms + bwd_ms, fwd_bytes + bwd_bytes
+        per_kernel = {"agg_fwd": {"ms": fwd_ms, "GB_s": fwd_bytes / fwd_ms / 1e6},
+                      "agg_bwd": {"ms": bwd_ms, "GB_s": bwd_bytes / bwd_ms / 1e6}}
+        dom, dom_ms, dom_bytes = "attn_agg_bwd_kernel (+ the dq partial sum)", bwd_ms, bwd_bytes
+        m_s = 64
+        xs = workloads.make_aggregation_inputs(m_s, H, C, d, seed=1)
+        cpu_fn = lambda: oracle.aggregation.backward(xs["q"], xs["k"], xs["v"], xs["dout"], 0.125)  # noqa: E731
+        cpu_bytes = nbytes * m_s // M
+        sample = f"fp64 forward+backward of {m_s} of the {M} patch positions"
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    dom_gbs = dom_bytes / (dom_ms * 1e-3) / 1e9
+    line = {
+        "metric": f"{args.row} HBM throughput", "value": gbs, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": 2, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": {"ulysses": "u8"}.get(args.row, "f32"), "data": "synthetic",
+        "config": {"workload": ROW_DOC[args.row]},
+        "roofline": {"bound": "hbm", "achieved": dom_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": dom_gbs / PEAK_HBM_GBS, "traffic": stored_traffic(dom.split()[0], args.row, args.row),
+                     "kernel": dom, "algorithmic_bytes": dom_bytes},
+        "per_kernel": per_kernel,
+        "kernel_sources": kernel_sources_digest(args.row),
+    }
+    if not args.no_cpu_baseline:
+        n, dt = timed_cpu(cpu_fn, budget)
+        # these oracles are element-wise numpy and einsum without BLAS: one thread
+        line["cpu_baseline"] = {"value": n * cpu_bytes / dt / 1e9, "unit": "GB/s", "cores": 1,
+                                "kind": "oracle", "sample": f"{sample}, {n} times in {dt:.1f} s"}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.row != "attention":
+        if args.gpus != 1:
+            print(json.dumps({"error": "this build runs on one GPU only", "n_gpus": args.gpus}))
+            sys.exit(2)
+        bench_row(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
@@ -317,7 +478,7 @@ def main():
         "kernels": per_kernel,
         "wall_s_timed": wall,
         "roofline": roof,
-        "kernel_sources": kernel_sources_digest(),
+        "kernel_sources": kernel_sources_digest(args.row),
     }
     if not args.no_cpu_baseline:
         print(f"# timing the oracle for ~{args.cpu_seconds:.0f} s", file=sys.stderr, flush=True)

@@ -188,7 +188,8 @@ int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, flo
  *
  * y is the contiguous [B][Hl][N][row] input (or output) of the attention
  * entry points. The collective itself is not part of this library.
- *   B, Nl, H, P: >= 1 with H divisible by P, P*B <= 65535, Nl*row_bytes/16 < 2^31.
+ *   B, Nl, H, P: >= 1 with H divisible by P, B <= 65535, Nl*row_bytes/16 < 2^31
+ *                and ceil(Nl*row_bytes/4096)*H < 2^31.
  *   row_bytes  : a multiple of 16, >= 16.
  *   src, dst   : device pointers, 16-byte aligned, not overlapping
  *                (src == dst is rejected; partial overlap is not detected).

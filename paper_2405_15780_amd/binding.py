@@ -232,40 +232,48 @@ def _ulysses(status, dst):
     return dst
 
 
-def ulysses_pack(x, P):
-    """x [B, Nl, H, *row] -> send [P, B, H/P, Nl, *row] (head group p in chunk p)."""
+def _dst(out, shape, like):
+    """`out` if given (checked), else a new tensor of `shape` like `like`."""
     torch = _torch()
+    if out is None:
+        return torch.empty(shape, dtype=like.dtype, device=like.device)
+    if not (out.is_cuda and out.dtype == like.dtype and out.is_contiguous() and tuple(out.shape) == tuple(shape)):
+        raise TypeError(f"out must be a contiguous {like.dtype} CUDA tensor of shape {tuple(shape)}")
+    return out
+
+
+def ulysses_pack(x, P, out=None):
+    """x [B, Nl, H, *row] -> send [P, B, H/P, Nl, *row] (head group p in chunk p)."""
     (B, Nl, H), row, rb = _rows(x, 3, "x")
-    send = torch.empty((P, B, H // P, Nl) + row, dtype=x.dtype, device=x.device)
+    if P < 1 or H % P != 0:
+        raise ValueError("H must be a multiple of P")
+    send = _dst(out, (P, B, H // P, Nl) + row, x)
     return _ulysses(library().vitattn_ulysses_pack(x.data_ptr(), send.data_ptr(), B, Nl, H, P, rb, _stream_ptr(x)),
                     send)
 
 
-def ulysses_unpack(recv):
+def ulysses_unpack(recv, out=None):
     """recv [P, B, Hl, Nl, *row] (chunk r from rank r) -> y [B, Hl, P*Nl, *row]."""
-    torch = _torch()
     (P, B, Hl, Nl), row, rb = _rows(recv, 4, "recv")
-    y = torch.empty((B, Hl, P * Nl) + row, dtype=recv.dtype, device=recv.device)
+    y = _dst(out, (B, Hl, P * Nl) + row, recv)
     return _ulysses(library().vitattn_ulysses_unpack(recv.data_ptr(), y.data_ptr(), B, Nl, Hl * P, P, rb,
                                                      _stream_ptr(recv)), y)
 
 
-def ulysses_pack_out(y, P):
+def ulysses_pack_out(y, P, out=None):
     """y [B, Hl, P*Nl, *row] -> send [P, B, Hl, Nl, *row] (the inverse of unpack)."""
-    torch = _torch()
     (B, Hl, N), row, rb = _rows(y, 3, "y")
-    if N % P != 0:
+    if P < 1 or N % P != 0:
         raise ValueError("the sequence length must be divisible by P")
-    send = torch.empty((P, B, Hl, N // P) + row, dtype=y.dtype, device=y.device)
+    send = _dst(out, (P, B, Hl, N // P) + row, y)
     return _ulysses(library().vitattn_ulysses_pack_out(y.data_ptr(), send.data_ptr(), B, N // P, Hl * P, P, rb,
                                                        _stream_ptr(y)), send)
 
 
-def ulysses_unpack_out(recv):
+def ulysses_unpack_out(recv, out=None):
     """recv [P, B, Hl, Nl, *row] -> x [B, Nl, P*Hl, *row] (the inverse of pack)."""
-    torch = _torch()
     (P, B, Hl, Nl), row, rb = _rows(recv, 4, "recv")
-    x = torch.empty((B, Nl, P * Hl) + row, dtype=recv.dtype, device=recv.device)
+    x = _dst(out, (B, Nl, P * Hl) + row, recv)
     return _ulysses(library().vitattn_ulysses_unpack_out(recv.data_ptr(), x.data_ptr(), B, Nl, Hl * P, P, rb,
                                                          _stream_ptr(recv)), x)
 

@@ -14,9 +14,11 @@
 // and their dot products are lane-per-key (a lane reads its whole key row);
 // the weighted sums over keys are lane-per-column (each V, K, dK, dV row is
 // one coalesced 64-lane access) with the key's probability broadcast by
-// readlane. dq is reduced without atomics: each block sums a fixed range of
-// patches into a partial in the workspace, then one pass adds the partials
-// in order, so results are bitwise reproducible.
+// readlane. Those sums take keys in groups of G, loading the group's rows
+// before using any, so that a wave has G row loads in flight rather than one.
+// dq is reduced without atomics: each block sums a fixed range of patches
+// into a partial in the workspace, then one pass adds the partials in a fixed
+// order, so results are bitwise reproducible.
 #include <math.h>
 
 #include "vitattn_common.h"
@@ -48,7 +50,7 @@ __device__ __forceinline__ float row_dot(const uint16_t* row, const float* x) {
   const uint4* r = reinterpret_cast<const uint4*>(row);
   const float4* xv = reinterpret_cast<const float4*>(x);
   float acc = 0.f;
-#pragma unroll 4
+#pragma unroll
   for (int t = 0; t < D / 8; ++t) {
     const uint4 w = r[t];
     const float4 a = xv[2 * t], b = xv[2 * t + 1];
@@ -118,12 +120,23 @@ __global__ __launch_bounds__(256) void attn_agg_fwd_kernel(const uint16_t* __res
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] *= alpha;
     const int n = min(64, C - c0);
-    for (int j = 0; j < n; ++j) {
+    const auto key = [&](int j, const float (&vc)[E]) {
       const float pj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p), j));
-      float vc[E];
-      row_cols<D>(vb + (size_t)(c0 + j) * D, lane, vc);
 #pragma unroll
       for (int e = 0; e < E; ++e) acc[e] = fmaf(pj, vc[e], acc[e]);
+    };
+    int j = 0;
+    for (; j + kAggGroup <= n; j += kAggGroup) {
+      float vc[kAggGroup][E];
+#pragma unroll
+      for (int u = 0; u < kAggGroup; ++u) row_cols<D>(vb + (size_t)(c0 + j + u) * D, lane, vc[u]);
+#pragma unroll
+      for (int u = 0; u < kAggGroup; ++u) key(j + u, vc[u]);
+    }
+    for (; j < n; ++j) {
+      float vc[E];
+      row_cols<D>(vb + (size_t)(c0 + j) * D, lane, vc);
+      key(j, vc);
     }
     m_run = m_new;
   }
@@ -181,18 +194,29 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
         ds = p * (row_dot<D>(vb + (size_t)c * D, gx) - Dm);
       }
       const int n = min(64, C - c0);
-      for (int j = 0; j < n; ++j) {
+      const auto key = [&](int j, const float (&kc)[E]) {
         const float pj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p), j));
         const float dsj = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ds), j));
         const size_t row = (size_t)(c0 + j) * D;
-        float kc[E];
-        row_cols<D>(kb + row, lane, kc);
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           dkb[row + lane * E + e] = scale * dsj * qx[lane * E + e];
           dvb[row + lane * E + e] = pj * g[e];
           dq[e] = fmaf(dsj, kc[e], dq[e]);
         }
+      };
+      int j = 0;
+      for (; j + kAggGroup <= n; j += kAggGroup) {
+        float kc[kAggGroup][E];
+#pragma unroll
+        for (int u = 0; u < kAggGroup; ++u) row_cols<D>(kb + (size_t)(c0 + j + u) * D, lane, kc[u]);
+#pragma unroll
+        for (int u = 0; u < kAggGroup; ++u) key(j + u, kc[u]);
+      }
+      for (; j < n; ++j) {
+        float kc[E];
+        row_cols<D>(kb + (size_t)(c0 + j) * D, lane, kc);
+        key(j, kc);
       }
     }
   }
@@ -205,14 +229,27 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
   }
 }
 
-// dq[h][e] = scale * sum over chunks, in chunk order
+// dq[t] = scale * the sum over chunks of partial[chunk][t], t = h*D + e. A
+// block takes 16 columns; its thread (r, col) sums chunks r, r+16, r+32, ...
+// in that order, then thread (0, col) adds the 16 sums in order of r.
 __global__ __launch_bounds__(256) void attn_agg_dq_kernel(const float* __restrict__ partial, float* __restrict__ dq,
                                                           int chunks, int HD, float scale) {
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  if (t >= HD) return;
+  __shared__ float red[16][17];
+  const int col = threadIdx.x & 15, r = threadIdx.x >> 4;
+  const int t = blockIdx.x * 16 + col;
   float s = 0.f;
-  for (int c = 0; c < chunks; ++c) s += partial[(size_t)c * HD + t];
-  dq[t] = scale * s;
+  if (t < HD) {
+#pragma unroll 8
+    for (int c = r; c < chunks; c += 16) s += partial[(size_t)c * HD + t];
+  }
+  red[r][col] = s;
+  __syncthreads();
+  if (r == 0 && t < HD) {
+    float tot = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tot += red[i][col];
+    dq[t] = scale * tot;
+  }
 }
 
 #define VITATTN_AGG_INSTANTIATE(D)                                                                             \
@@ -227,7 +264,12 @@ VITATTN_AGG_INSTANTIATE(64)
 VITATTN_AGG_INSTANTIATE(128)
 #undef VITATTN_AGG_INSTANTIATE
 
-int agg_chunks(int M) { return M < kAggMaxChunks ? M : kAggMaxChunks; }
+// blocks along M in the backward pass: about kAggTargetBlocks blocks in all
+int agg_chunks(int M, int H) {
+  const int target = kAggTargetBlocks / H > 1 ? kAggTargetBlocks / H : 1;
+  const int c = target < kAggMaxChunks ? target : kAggMaxChunks;
+  return M < c ? M : c;
+}
 
 template <int D>
 static hipError_t agg_fwd_d(const AggArgs& a) {
@@ -239,14 +281,14 @@ static hipError_t agg_fwd_d(const AggArgs& a) {
 
 template <int D>
 static hipError_t agg_bwd_d(const AggArgs& a) {
-  const int chunks = agg_chunks(a.M);
+  const int chunks = agg_chunks(a.M, a.H);
   const int per = (a.M + chunks - 1) / chunks;
   hipLaunchKernelGGL(attn_agg_bwd_kernel<D>, dim3((unsigned)chunks, (unsigned)a.H), dim3(256), 0, a.stream, a.q, a.k,
                      a.v, a.o, a.dout, a.lse, a.dk, a.dv, a.partial, a.M, a.H, a.C, per, a.scale * kLog2e, a.scale);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int HD = a.H * D;
-  hipLaunchKernelGGL(attn_agg_dq_kernel, dim3((unsigned)((HD + 255) / 256)), dim3(256), 0, a.stream, a.partial, a.dq,
+  hipLaunchKernelGGL(attn_agg_dq_kernel, dim3((unsigned)((HD + 15) / 16)), dim3(256), 0, a.stream, a.partial, a.dq,
                      chunks, HD, a.scale);
   return hipGetLastError();
 }

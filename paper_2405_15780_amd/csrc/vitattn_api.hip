@@ -239,8 +239,9 @@ static int ulysses(const void* src, void* dst, int B, int Nl, int H, int P, int 
     if (B < 1 || Nl < 1 || H < 1 || P < 1 || H % P != 0) return VITATTN_E_INVAL;
     if (row_bytes < 16 || row_bytes % 16 != 0) return VITATTN_E_INVAL;
     if (!aligned16(src) || !aligned16(dst) || src == dst) return VITATTN_E_INVAL;
-    // grid limits: P*B and H/P index grid dimensions, Nl*row_bytes/16 a 32-bit thread index
-    if ((long long)P * B > 65535 || (long long)Nl * (row_bytes / 16) > 0x7fffffffLL) return VITATTN_E_INVAL;
+    // grid limits: B indexes grid.y, (token tiles x H) grid.x, Nl*row_bytes/16 a 32-bit thread index
+    if (B > 65535 || (long long)Nl * (row_bytes / 16) > 0x7fffffffLL) return VITATTN_E_INVAL;
+    if (vitattn::ulysses_blocks(Nl, H, row_bytes) > 0x7fffffffL) return VITATTN_E_INVAL;
     if ((double)B * Nl * H * row_bytes > 9.0e18) return VITATTN_E_INVAL;
     vitattn::UlyssesArgs a;
     a.src = src;
@@ -285,7 +286,7 @@ static int check_agg(int M, int H, int C, int d, float scale) {
 
 size_t vitattn_agg_bwd_workspace_bytes(int M, int H, int C, int d) {
   if (check_agg(M, H, C, d, 1.f) != VITATTN_OK) return 0;
-  return (size_t)vitattn::agg_chunks(M) * H * d * sizeof(float);
+  return (size_t)vitattn::agg_chunks(M, H) * H * d * sizeof(float);
 }
 
 int vitattn_agg_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int M, int H, int C, int d,

@@ -69,10 +69,13 @@ struct UlyssesArgs {
   hipStream_t stream;
 };
 hipError_t launch_ulysses(const UlyssesArgs& a);
+long ulysses_blocks(int Nl, int H, int row_bytes);  // grid.x of the layout kernels
 
 // Channel aggregation (attention of one learnable query per head over the C
 // channel tokens of each of M patches); see vitattn_agg.hip.
-constexpr int kAggMaxChunks = 1024;  // blocks along M in the backward pass (dq partials)
+constexpr int kAggMaxChunks = 1024;      // most blocks along M in the backward pass (dq partials)
+constexpr int kAggTargetBlocks = 8192;  // backward blocks (chunks x heads) aimed for
+constexpr int kAggGroup = 16;           // keys whose rows one wave loads together
 struct AggArgs {
   const uint16_t* q;     // [H][d]
   const uint16_t* k;     // [M][H][C][d]
@@ -90,7 +93,7 @@ struct AggArgs {
   float scale;
   hipStream_t stream;
 };
-int agg_chunks(int M);
+int agg_chunks(int M, int H);
 hipError_t launch_agg_fwd(const AggArgs& a);
 hipError_t launch_agg_bwd(const AggArgs& a);
 

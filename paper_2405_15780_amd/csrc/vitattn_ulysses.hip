@@ -9,9 +9,11 @@
 //   U  attention layout [B][Hl][P*Nl]     row (b*Hl + j)*(P*Nl) + p*Nl + i
 // pack: A -> C (send buffer), unpack: C -> U (after the all-to-all, recv
 // chunk p came from rank p), pack_out: U -> C, unpack_out: C -> A.
-// Pure copies, bound by HBM bandwidth; one 16-byte vector per thread, and the
-// block-uniform indices (b, j, p) come from the grid so that each thread
-// divides only once.
+// Pure copies, bound by HBM bandwidth; one 16-byte vector per thread. A
+// block copies 256 vectors of consecutive tokens of one head, and consecutive
+// blocks take consecutive heads of the same tokens, so that the blocks in
+// flight together sweep whole [H][row] token records of the sequence-major
+// side instead of one row out of every H.
 #include "vitattn_common.h"
 #include "vitattn_launch.h"
 
@@ -20,13 +22,14 @@ namespace vitattn {
 template <int MODE>
 __global__ __launch_bounds__(256) void ulysses_layout_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
                                                              int B, int Nl, int H, int P, int vpr) {
-  const int idx = blockIdx.x * 256 + threadIdx.x;
+  const int hh = blockIdx.x % H;  // global head p*Hl + j
+  const int idx = (blockIdx.x / H) * 256 + threadIdx.x;
   if (idx >= Nl * vpr) return;
   const int i = idx / vpr, v = idx - (idx / vpr) * vpr;
-  const int j = blockIdx.y;
-  const int p = blockIdx.z / B, b = blockIdx.z - (blockIdx.z / B) * B;
   const int Hl = H / P;
-  const long rowA = ((long)b * Nl + i) * H + (long)p * Hl + j;
+  const int p = hh / Hl, j = hh - (hh / Hl) * Hl;
+  const int b = blockIdx.y;
+  const long rowA = ((long)b * Nl + i) * H + hh;
   const long rowC = (((long)p * B + b) * Hl + j) * Nl + i;
   const long rowU = ((long)b * Hl + j) * ((long)P * Nl) + (long)p * Nl + i;
   long rs, rd;
@@ -42,10 +45,12 @@ __global__ __launch_bounds__(256) void ulysses_layout_kernel(const uint4* __rest
   dst[rd * vpr + v] = src[rs * vpr + v];
 }
 
+long ulysses_blocks(int Nl, int H, int row_bytes) { return ((long)Nl * (row_bytes / 16) + 255) / 256 * H; }
+
 template <int MODE>
 static hipError_t layout_m(const UlyssesArgs& a) {
   const int vpr = a.row_bytes / 16;
-  const dim3 grid((unsigned)(((long)a.Nl * vpr + 255) / 256), (unsigned)(a.H / a.P), (unsigned)(a.P * a.B));
+  const dim3 grid((unsigned)ulysses_blocks(a.Nl, a.H, a.row_bytes), (unsigned)a.B);
   hipLaunchKernelGGL(ulysses_layout_kernel<MODE>, grid, dim3(256), 0, a.stream, static_cast<const uint4*>(a.src),
                      static_cast<uint4*>(a.dst), a.B, a.Nl, a.H, a.P, vpr);
   return hipGetLastError();

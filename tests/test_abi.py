@@ -216,7 +216,8 @@ def test_merge_rejects_bad_arguments(kw, expected):
                                   "vitattn_ulysses_unpack_out"])
 @pytest.mark.parametrize("kw", [dict(H=6, P=4), dict(P=0), dict(B=0), dict(Nl=0), dict(row_bytes=24),
                                 dict(row_bytes=0), dict(src=None), dict(dst=None), dict(src="dst"),
-                                dict(src=4100), dict(B=40000, P=2, H=2)])
+                                dict(src=4100), dict(B=70000, P=2, H=2),
+                                dict(Nl=1 << 24, H=1 << 16, P=1, row_bytes=16)])
 def test_ulysses_layouts_reject_bad_arguments(name, kw):
     b = Bufs()
     args = dict(src=b.p(0), dst=b.p(1), B=1, Nl=4, H=4, P=2, row_bytes=32)
