@@ -23,11 +23,17 @@
  *    never allocates, frees or retains them, and holds no per-call state.
  *  - Tensors are contiguous row-major [B][H][N][d] (d innermost); lse and the
  *    backward workspace are [B][H][N]. Element offsets use 64-bit arithmetic.
+ *    vitattn_fwd_strided / vitattn_bwd_strided take any batch, head and row
+ *    strides instead (e.g. the sequence-major [B][N][H][d] layout), see
+ *    vitattn_strides below.
  *  - q, k, v and dout hold bfloat16 values as raw 16-bit patterns. o, lse, dq,
  *    dk and dv are fp32. Every pointer must be 16-byte aligned.
- *  - Supported head dims: d = 64 and d = 128. Any N >= 1 with (N + 256)*d*2
- *    below 2^31 (the kernels address one head's rows with 32-bit offsets;
- *    N up to 8,388,351 at d = 128) and B*H*N below 2^31.
+ *  - Supported head dims: any multiple of 8 from 8 to 160 (the paper's models
+ *    use 64, 72, 128 and 160, Table I and Sec. V-C). The kernels compute in
+ *    tiles of width 64, 96, 128 or 160 with the columns past d zero, so d = 72
+ *    costs what d = 96 costs. Any N >= 1 with (N + 256) * row_stride * 2 below
+ *    2^31 for every bf16 operand (the kernels address one head's rows with
+ *    32-bit offsets; N up to 8,388,351 for dense d = 128) and B*H*N below 2^31.
  *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *    the call returns without waiting. Execution faults surface at the
  *    caller's next synchronisation on that stream.
@@ -49,7 +55,7 @@ extern "C" {
 enum vitattn_status {
   VITATTN_OK = 0,
   VITATTN_E_INVAL = 1,       /* null/misaligned pointer, B/H/N < 1, non-finite or non-positive scale, size overflow */
-  VITATTN_E_UNSUPPORTED = 2, /* d not in {64, 128} */
+  VITATTN_E_UNSUPPORTED = 2, /* head dim d not supported (see above; vitattn_merge: d in {64, 128}) */
   VITATTN_E_WORKSPACE = 3,   /* workspace missing or smaller than vitattn_bwd_workspace_bytes() */
   VITATTN_E_HIP = 4,         /* the HIP runtime reported an error when launching */
   VITATTN_E_INTERNAL = 5     /* unexpected internal failure */
@@ -155,6 +161,40 @@ int vitattn_fwd_kv(const void* q, const void* k, const void* v, float* o, float*
 int vitattn_bwd_kv(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
                    float* dq, float* dk, float* dv, int B, int H, int Nq, int Nk, int d, float scale, int flags,
                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Operands in other layouts. The layout an all-to-all or a fused QKV
+ * projection produces is rarely the dense [B][H][N][d]: the sequence-major
+ * [B][N][H][d] (paper Sec. II "Sequence Parallel") has strides
+ * {N*H*d, d, H*d}, rows padded to a larger pitch have row > d, and a slice
+ * of a [B][N][3][H][d] QKV tensor has row = 3*H*d. The kernels read and write
+ * such operands in place; no copy is made.
+ *
+ * Element strides of one operand viewed as [B][H][N][d]; the d elements of a
+ * row are contiguous. Every stride must be >= 0 and a multiple of 8 elements
+ * for bf16 operands (4 for fp32), so rows stay 16-byte aligned, and
+ * row >= d. Inputs may repeat a head or batch (stride 0, e.g. keys shared by
+ * several query heads); an output may not overlap itself (checked: sorted by
+ * stride, every dimension must step past the span of the smaller ones). Each
+ * bf16 operand needs (rows + 256) * row * 2 < 2^31. Violations:
+ * VITATTN_E_INVAL. lse and the workspace stay dense [B][H][Nq].
+ */
+typedef struct vitattn_strides {
+  long long batch, head, row;
+} vitattn_strides;
+
+/* vitattn_fwd_kv with a layout per operand (same computation and validation). */
+int vitattn_fwd_strided(const void* q, vitattn_strides sq, const void* k, vitattn_strides sk, const void* v,
+                        vitattn_strides sv, float* o, vitattn_strides so, float* lse, int B, int H, int Nq, int Nk,
+                        int d, float scale, void* stream);
+
+/* vitattn_bwd_kv with a layout per operand (same computation, flags and
+ * validation); sdo is the layout of dout. */
+int vitattn_bwd_strided(const void* q, vitattn_strides sq, const void* k, vitattn_strides sk, const void* v,
+                        vitattn_strides sv, const float* o, vitattn_strides so, const void* dout,
+                        vitattn_strides sdo, const float* lse, float* dq, vitattn_strides sdq, float* dk,
+                        vitattn_strides sdk, float* dv, vitattn_strides sdv, int B, int H, int Nq, int Nk, int d,
+                        float scale, int flags, void* workspace, size_t workspace_bytes, void* stream);
 
 /* largest number of partial results vitattn_merge accepts */
 #define VITATTN_MERGE_MAX_PARTS 65536

@@ -9,6 +9,7 @@ fallback path.
 from .binding import (  # noqa: F401
     LIB_PATH,
     VITATTN_BWD_ACCUMULATE_DQ,
+    Strides,
     VitattnError,
     agg_bwd,
     agg_fwd,
@@ -20,6 +21,7 @@ from .binding import (  # noqa: F401
     library,
     merge,
     status_str,
+    strides_of,
     ulysses_pack,
     ulysses_pack_out,
     ulysses_unpack,

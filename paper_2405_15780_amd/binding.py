@@ -19,6 +19,14 @@ _lib = None
 
 c_int, c_float, c_size_t, c_void_p = ctypes.c_int, ctypes.c_float, ctypes.c_size_t, ctypes.c_void_p
 
+
+class Strides(ctypes.Structure):
+    """vitattn_strides: element strides of an operand viewed as [B, H, N, d]."""
+    _fields_ = [("batch", ctypes.c_longlong), ("head", ctypes.c_longlong), ("row", ctypes.c_longlong)]
+
+
+_S = Strides
+
 _SIGNATURES = {
     "vitattn_fwd": (c_int, [c_void_p] * 5 + [c_int] * 4 + [c_float, c_void_p]),
     "vitattn_bwd_workspace_bytes": (c_size_t, [c_int] * 4),
@@ -28,6 +36,9 @@ _SIGNATURES = {
     "vitattn_bwd_dq": (c_int, [c_void_p] * 6 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
     "vitattn_fwd_kv": (c_int, [c_void_p] * 5 + [c_int] * 5 + [c_float, c_void_p]),
     "vitattn_bwd_kv": (c_int, [c_void_p] * 9 + [c_int] * 5 + [c_float, c_int, c_void_p, c_size_t, c_void_p]),
+    "vitattn_fwd_strided": (c_int, [c_void_p, _S] * 4 + [c_void_p] + [c_int] * 5 + [c_float, c_void_p]),
+    "vitattn_bwd_strided": (c_int, [c_void_p, _S] * 5 + [c_void_p] + [c_void_p, _S] * 3 + [c_int] * 5
+                            + [c_float, c_int, c_void_p, c_size_t, c_void_p]),
     "vitattn_merge": (c_int, [c_void_p] * 2 + [c_int] + [c_void_p] * 2 + [c_int] * 4 + [c_void_p]),
     "vitattn_agg_fwd": (c_int, [c_void_p] * 5 + [c_int] * 4 + [c_float, c_void_p]),
     "vitattn_agg_bwd_workspace_bytes": (c_size_t, [c_int] * 4),
@@ -93,9 +104,19 @@ def _stream_ptr(t) -> int:
 
 def _as_input(t, name):
     torch = _torch()
-    if not (t.is_cuda and t.dtype == torch.bfloat16 and t.dim() == 4 and t.is_contiguous()):
-        raise TypeError(f"{name} must be a contiguous 4-D bfloat16 CUDA tensor [B, H, N, d]")
+    if not (t.is_cuda and t.dtype == torch.bfloat16 and t.dim() == 4 and (t.shape[3] == 1 or t.stride(3) == 1)):
+        raise TypeError(f"{name} must be a 4-D bfloat16 CUDA tensor [B, H, N, d] with unit stride along d "
+                        "(other strides are free, e.g. a [B, N, H, d] tensor passed as .transpose(1, 2))")
     return t
+
+
+def strides_of(t):
+    """vitattn_strides of a [B, H, N, d] view (d contiguous)."""
+    return Strides(t.stride(0), t.stride(1), t.stride(2))
+
+
+def _dense(*ts):
+    return all(t.is_contiguous() for t in ts)
 
 
 def _default_scale(d, scale):
@@ -125,7 +146,11 @@ def fwd(q, k, v, scale=None, out=None):
     else:
         o, lse = out
     lib = library()
-    if Nq == Nk:
+    if not _dense(q, k, v, o):
+        st = lib.vitattn_fwd_strided(q.data_ptr(), strides_of(q), k.data_ptr(), strides_of(k), v.data_ptr(),
+                                     strides_of(v), o.data_ptr(), strides_of(o), lse.data_ptr(), B, H, Nq, Nk, d,
+                                     _default_scale(d, scale), _stream_ptr(q))
+    elif Nq == Nk:
         st = lib.vitattn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), B, H, Nq, d,
                              _default_scale(d, scale), _stream_ptr(q))
     else:
@@ -161,7 +186,14 @@ def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None, accumulate_
     else:
         dq, dk, dv = out
     lib = library()
-    if Nq == Nk and not accumulate_dq:
+    if not _dense(q, k, v, o, dout, dq, dk, dv):
+        st = lib.vitattn_bwd_strided(q.data_ptr(), strides_of(q), k.data_ptr(), strides_of(k), v.data_ptr(),
+                                     strides_of(v), o.data_ptr(), strides_of(o), dout.data_ptr(), strides_of(dout),
+                                     lse.data_ptr(), dq.data_ptr(), strides_of(dq), dk.data_ptr(), strides_of(dk),
+                                     dv.data_ptr(), strides_of(dv), B, H, Nq, Nk, d, _default_scale(d, scale),
+                                     VITATTN_BWD_ACCUMULATE_DQ if accumulate_dq else 0, ws.data_ptr(), ws_bytes,
+                                     _stream_ptr(q))
+    elif Nq == Nk and not accumulate_dq:
         st = lib.vitattn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(), lse.data_ptr(),
                              dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, Nq, d, _default_scale(d, scale),
                              ws.data_ptr(), ws_bytes, _stream_ptr(q))

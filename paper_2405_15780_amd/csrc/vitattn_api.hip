@@ -10,21 +10,29 @@
 #include "../../include/vitattn.h"
 #include "vitattn_launch.h"
 
-#define VITATTN_VERSION "0.2.0"
+#define VITATTN_VERSION "0.3.0"
 
 namespace {
 
 bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-int check_sizes(int B, int H, int N, int d) {
+// head dims of the attention kernels: multiples of 8 (16-byte rows) up to 160
+bool head_dim_ok(int d) { return d >= 8 && d <= 160 && d % 8 == 0; }
+
+// row counts: row indices and grid sizes are 32-bit, so B*H*N must fit in an
+// int; per-head byte offsets of a dense bf16 operand (plus the padding rows of
+// the last tiles) must fit in 31 bits
+int check_rows(int B, int H, int N, int d) {
   if (B < 1 || H < 1 || N < 1) return VITATTN_E_INVAL;
-  if (d != 64 && d != 128) return VITATTN_E_UNSUPPORTED;
-  // row indices and grid sizes are 32-bit: B*H*N must fit in an int
-  const long long rows = (long long)B * H * N;
-  if (rows > 0x7fffffffLL) return VITATTN_E_INVAL;
-  // per-head byte offsets (plus one tile of padding) must fit in 31 bits
+  if ((long long)B * H * N > 0x7fffffffLL) return VITATTN_E_INVAL;
   if ((long long)(N + 256) * d * 2 > 0x7fffffffLL) return VITATTN_E_INVAL;
   return VITATTN_OK;
+}
+
+int check_sizes(int B, int H, int N, int d) {
+  if (B < 1 || H < 1 || N < 1) return VITATTN_E_INVAL;
+  if (!head_dim_ok(d)) return VITATTN_E_UNSUPPORTED;
+  return check_rows(B, H, N, d);
 }
 
 bool scale_ok(float s) { return isfinite(s) && s > 0.f; }
@@ -33,6 +41,50 @@ bool scale_ok(float s) { return isfinite(s) && s > 0.f; }
 int check_sizes_kv(int B, int H, int Nq, int Nk, int d) {
   const int st = check_sizes(B, H, Nq, d);
   return st != VITATTN_OK ? st : check_sizes(B, H, Nk, d);
+}
+
+// One operand's strides (elements). Rows must be 16-byte aligned and must not
+// overlap (row >= d); every stride is non-negative and a multiple of
+// 16 / elem_bytes elements. Operands read through buffer resources (the bf16
+// inputs) must keep (N + 256) rows within 31-bit byte offsets. An output must
+// not overlap itself: sorted by stride, each dimension must step past the
+// span of the smaller ones. Inputs may repeat heads or batches (stride 0).
+int check_map(const vitattn_strides& m, int B, int H, int N, int d, int elem_bytes, bool output) {
+  const long long unit = 16 / elem_bytes;
+  if (m.batch < 0 || m.head < 0 || m.row < d) return VITATTN_E_INVAL;
+  if (m.batch % unit != 0 || m.head % unit != 0 || m.row % unit != 0) return VITATTN_E_INVAL;
+  if (m.row > 0x7fffffffLL) return VITATTN_E_INVAL;
+  if (elem_bytes == 2 && (long long)(N + 256) * m.row * 2 > 0x7fffffffLL) return VITATTN_E_INVAL;
+  // the largest element offset must fit comfortably in 64 bits
+  if ((double)(B - 1) * m.batch + (double)(H - 1) * m.head + (double)N * m.row > 4.0e18) return VITATTN_E_INVAL;
+  if (output) {
+    long long size[3] = {B, H, N}, stride[3] = {m.batch, m.head, m.row};
+    int idx[3] = {0, 1, 2};
+    for (int i = 0; i < 3; ++i)  // sort the three dimensions by stride
+      for (int j = i + 1; j < 3; ++j)
+        if (stride[idx[j]] < stride[idx[i]]) {
+          const int t = idx[i];
+          idx[i] = idx[j];
+          idx[j] = t;
+        }
+    long long span = d;  // elements covered by the dimensions taken so far (a row first)
+    for (int i = 0; i < 3; ++i) {
+      const int x = idx[i];
+      if (size[x] == 1) continue;
+      if (stride[x] < span) return VITATTN_E_INVAL;
+      span += (size[x] - 1) * stride[x];
+    }
+  }
+  return VITATTN_OK;
+}
+
+vitattn::Map to_map(const vitattn_strides& m) { return vitattn::Map{m.batch, m.head, (int)m.row}; }
+vitattn_strides dense(int H, int N, int d) {
+  vitattn_strides m;
+  m.batch = (long long)H * N * d;
+  m.head = (long long)N * d;
+  m.row = d;
+  return m;
 }
 
 }  // namespace
@@ -50,7 +102,7 @@ const char* vitattn_status_str(int status) {
   switch (status) {
     case VITATTN_OK: return "VITATTN_OK";
     case VITATTN_E_INVAL: return "VITATTN_E_INVAL: invalid argument";
-    case VITATTN_E_UNSUPPORTED: return "VITATTN_E_UNSUPPORTED: head dim must be 64 or 128";
+    case VITATTN_E_UNSUPPORTED: return "VITATTN_E_UNSUPPORTED: unsupported head dim";
     case VITATTN_E_WORKSPACE: return "VITATTN_E_WORKSPACE: workspace missing or too small";
     case VITATTN_E_HIP: return "VITATTN_E_HIP: HIP runtime error at launch";
     case VITATTN_E_INTERNAL: return "VITATTN_E_INTERNAL: internal error";
@@ -72,18 +124,33 @@ int vitattn_fwd(const void* q, const void* k, const void* v, float* o, float* ls
 
 int vitattn_fwd_kv(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int Nq, int Nk,
                    int d, float scale, void* stream) {
+  return vitattn_fwd_strided(q, dense(H, Nq, d), k, dense(H, Nk, d), v, dense(H, Nk, d), o, dense(H, Nq, d), lse, B,
+                             H, Nq, Nk, d, scale, stream);
+}
+
+int vitattn_fwd_strided(const void* q, vitattn_strides sq, const void* k, vitattn_strides sk, const void* v,
+                        vitattn_strides sv, float* o, vitattn_strides so, float* lse, int B, int H, int Nq, int Nk,
+                        int d, float scale, void* stream) {
   try {
     int st = check_sizes_kv(B, H, Nq, Nk, d);
     if (st != VITATTN_OK) return st;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
       return VITATTN_E_INVAL;
     if (!scale_ok(scale)) return VITATTN_E_INVAL;
+    if (check_map(sq, B, H, Nq, d, 2, false) || check_map(sk, B, H, Nk, d, 2, false) ||
+        check_map(sv, B, H, Nk, d, 2, false) || check_map(so, B, H, Nq, d, 4, true))
+      return VITATTN_E_INVAL;
     vitattn::FwdArgs a;
     a.q = static_cast<const uint16_t*>(q);
     a.k = static_cast<const uint16_t*>(k);
     a.v = static_cast<const uint16_t*>(v);
     a.o = o;
     a.lse = lse;
+    a.mq = to_map(sq);
+    a.mk = to_map(sk);
+    a.mv = to_map(sv);
+    a.mo = to_map(so);
+    a.H = H;
     a.BH = B * H;
     a.Nq = Nq;
     a.Nk = Nk;
@@ -103,6 +170,7 @@ static int check_workspace(const void* ws, size_t bytes, int B, int H, int N, in
   return VITATTN_OK;
 }
 
+// Arguments of the backward kernels; operands without strides given are dense.
 static vitattn::BwdArgs bwd_args(const void* q, const void* k, const void* v, const float* o, const void* dout,
                                  const float* lse, float* dq, float* dk, float* dv, int B, int H, int Nq, int Nk,
                                  int d, float scale, bool accumulate_dq, const void* workspace, void* stream) {
@@ -118,6 +186,9 @@ static vitattn::BwdArgs bwd_args(const void* q, const void* k, const void* v, co
   a.dv = dv;
   a.drow = static_cast<float*>(const_cast<void*>(workspace));
   a.lse2 = a.drow + vitattn::bwd_region_floats((long long)B * H * Nq);
+  a.mq = a.mo = a.mg = a.mdq = to_map(dense(H, Nq, d));
+  a.mk = a.mv = a.mdk = a.mdv = to_map(dense(H, Nk, d));
+  a.H = H;
   a.BH = B * H;
   a.Nq = Nq;
   a.Nk = Nk;
@@ -138,6 +209,16 @@ int vitattn_bwd(const void* q, const void* k, const void* v, const float* o, con
 int vitattn_bwd_kv(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
                    float* dq, float* dk, float* dv, int B, int H, int Nq, int Nk, int d, float scale, int flags,
                    void* workspace, size_t workspace_bytes, void* stream) {
+  const vitattn_strides mq = dense(H, Nq, d), mk = dense(H, Nk, d);
+  return vitattn_bwd_strided(q, mq, k, mk, v, mk, o, mq, dout, mq, lse, dq, mq, dk, mk, dv, mk, B, H, Nq, Nk, d,
+                             scale, flags, workspace, workspace_bytes, stream);
+}
+
+int vitattn_bwd_strided(const void* q, vitattn_strides sq, const void* k, vitattn_strides sk, const void* v,
+                        vitattn_strides sv, const float* o, vitattn_strides so, const void* dout,
+                        vitattn_strides sdo, const float* lse, float* dq, vitattn_strides sdq, float* dk,
+                        vitattn_strides sdk, float* dv, vitattn_strides sdv, int B, int H, int Nq, int Nk, int d,
+                        float scale, int flags, void* workspace, size_t workspace_bytes, void* stream) {
   try {
     int st = check_sizes_kv(B, H, Nq, Nk, d);
     if (st != VITATTN_OK) return st;
@@ -146,10 +227,23 @@ int vitattn_bwd_kv(const void* q, const void* k, const void* v, const float* o, 
       return VITATTN_E_INVAL;
     if (!scale_ok(scale)) return VITATTN_E_INVAL;
     if ((flags & ~VITATTN_BWD_ACCUMULATE_DQ) != 0) return VITATTN_E_INVAL;
+    if (check_map(sq, B, H, Nq, d, 2, false) || check_map(sk, B, H, Nk, d, 2, false) ||
+        check_map(sv, B, H, Nk, d, 2, false) || check_map(so, B, H, Nq, d, 4, false) ||
+        check_map(sdo, B, H, Nq, d, 2, false) || check_map(sdq, B, H, Nq, d, 4, true) ||
+        check_map(sdk, B, H, Nk, d, 4, true) || check_map(sdv, B, H, Nk, d, 4, true))
+      return VITATTN_E_INVAL;
     st = check_workspace(workspace, workspace_bytes, B, H, Nq, d);
     if (st != VITATTN_OK) return st;
-    const vitattn::BwdArgs a = bwd_args(q, k, v, o, dout, lse, dq, dk, dv, B, H, Nq, Nk, d, scale,
-                                        (flags & VITATTN_BWD_ACCUMULATE_DQ) != 0, workspace, stream);
+    vitattn::BwdArgs a = bwd_args(q, k, v, o, dout, lse, dq, dk, dv, B, H, Nq, Nk, d, scale,
+                                  (flags & VITATTN_BWD_ACCUMULATE_DQ) != 0, workspace, stream);
+    a.mq = to_map(sq);
+    a.mk = to_map(sk);
+    a.mv = to_map(sv);
+    a.mo = to_map(so);
+    a.mg = to_map(sdo);
+    a.mdq = to_map(sdq);
+    a.mdk = to_map(sdk);
+    a.mdv = to_map(sdv);
     return vitattn::launch_bwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
   } catch (...) {
     return VITATTN_E_INTERNAL;
@@ -159,7 +253,9 @@ int vitattn_bwd_kv(const void* q, const void* k, const void* v, const float* o, 
 int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, float* o, float* lse, int B, int H,
                   int N, int d, void* stream) {
   try {
-    int st = check_sizes(B, H, N, d);
+    if (B < 1 || H < 1 || N < 1) return VITATTN_E_INVAL;
+    if (d != 64 && d != 128) return VITATTN_E_UNSUPPORTED;
+    int st = check_rows(B, H, N, d);
     if (st != VITATTN_OK) return st;
     if (n_parts < 1 || n_parts > VITATTN_MERGE_MAX_PARTS) return VITATTN_E_INVAL;
     if (!aligned16(o_parts) || !aligned16(lse_parts) || !aligned16(o) || !aligned16(lse)) return VITATTN_E_INVAL;

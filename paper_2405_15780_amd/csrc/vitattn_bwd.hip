@@ -11,7 +11,9 @@
 //      registers); streams K and V in tiles of 64 keys:
 //        S^T = K Q^T, P^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T
 // Splitting dQ from dK/dV costs one extra recomputation of S and dP but needs
-// no atomics, so results are deterministic.
+// no atomics, so results are deterministic. As in the forward pass, operands
+// may have any batch / head / row strides, and a head dim d below the tile
+// width D is padded with zero columns on load and cut off on store.
 #include <type_traits>
 
 #include "vitattn_common.h"
@@ -26,20 +28,24 @@ constexpr int kBwdThreads = 64 * kBwdWaves;
 
 // Writes the two per-row statistics the backward kernels stream: D_i =
 // sum_c dO_ic O_ic and LSE_i * log2(e) (the logsumexp in the base-2 units of
-// the kernels' exp2). Each lives in its own region of the workspace.
-template <int D>
+// the kernels' exp2). Each lives in its own region of the workspace. LPR
+// lanes per row take 8 columns each (lanes past the head dim add nothing).
+template <int LPR>
 __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __restrict__ dout,
                                                               const float* __restrict__ o,
                                                               const float* __restrict__ lse, float* __restrict__ drow,
-                                                              float* __restrict__ lse2, long rows) {
-  constexpr int LPR = D / 8;  // lanes per row, 8 elements each
-  const long row = (long)blockIdx.x * (256 / LPR) + threadIdx.x / LPR;
+                                                              float* __restrict__ lse2, const Map mg, const Map mo,
+                                                              int H, int N, int dr, int rows) {
+  const int row = blockIdx.x * (256 / LPR) + threadIdx.x / LPR;
   const int part = threadIdx.x % LPR;
   float acc = 0.f;
-  if (row < rows) {
-    const uint4 g = *reinterpret_cast<const uint4*>(dout + row * D + part * 8);
-    const float4 o0 = *reinterpret_cast<const float4*>(o + row * D + part * 8);
-    const float4 o1 = *reinterpret_cast<const float4*>(o + row * D + part * 8 + 4);
+  if (row < rows && part * 8 < dr) {
+    const int bh = row / N, n = row - bh * N;
+    const uint16_t* gp = dout + mg.head(bh, H) + (long long)n * mg.ld + part * 8;
+    const float* op = o + mo.head(bh, H) + (long long)n * mo.ld + part * 8;
+    const uint4 g = *reinterpret_cast<const uint4*>(gp);
+    const float4 o0 = *reinterpret_cast<const float4*>(op);
+    const float4 o1 = *reinterpret_cast<const float4*>(op + 4);
     const bf16x8 gb = as_bf16x8(g);
     acc = (float)gb[0] * o0.x + (float)gb[1] * o0.y + (float)gb[2] * o0.z + (float)gb[3] * o0.w +
           (float)gb[4] * o1.x + (float)gb[5] * o1.y + (float)gb[6] * o1.z + (float)gb[7] * o1.w;
@@ -93,11 +99,12 @@ template <int D>
 __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
-    float* __restrict__ dk, float* __restrict__ dv, int Nq, int Nk, int n_ktiles, int total, float c, float scale) {
+    float* __restrict__ dk, float* __restrict__ dv, const Map mq, const Map mk, const Map mv, const Map mg,
+    const Map mdk, const Map mdv, int H, int dr, int Nq, int Nk, int n_ktiles, int total, float c, float scale) {
   constexpr int KK = D / 16, NCB = D / 32;
   constexpr int PH = KK;           // ops per phase
   constexpr int NOPS = 4 * PH;     // ops per tile
-  constexpr int RPS = 16 / PH;     // query rows of vector work per op slot
+  // query rows of vector work: row r rides on op slot r * PH / 16 of its phase
   constexpr int TILE_BYTES = kDkvBQ * D * 2;
   constexpr int RING = 3;
   constexpr int NWAVES = 2 * kBwdWaves;
@@ -116,8 +123,13 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   char* const qbuf[RING] = {qbuf0, qbuf1, qbuf2};
   char* const gbuf[RING] = {gbuf0, gbuf1, gbuf2};
   float* const sbuf[RING] = {sbuf0, sbuf1, sbuf2};
-  // P exchange: [slot][key block][query block][contraction step][lane] of 8 bf16
-  __shared__ __attribute__((aligned(16))) uint4 xbuf[RING][kBwdWaves][2][2][64];
+  // P exchange: [slot][key block][query block][contraction step][lane] of 8
+  // bf16. Role P writes tile t's P at the end of iteration t and role dS reads
+  // it at the start of iteration t+1, so two slots (by tile parity) suffice;
+  // the narrower tiles use the ring slot instead, a compile-time index. The
+  // widest tile needs the two-slot form to fit in LDS.
+  constexpr int XR = D == 160 ? 2 : RING;
+  __shared__ __attribute__((aligned(16))) uint4 xbuf[XR][kBwdWaves][2][2][64];
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_ktiles;
@@ -128,22 +140,25 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   const bool role_p = wave < 4;
 
   // queries, dO and the row statistics have Nq rows per (b, h); K, V, dK, dV have Nk
-  const size_t head_off = (size_t)bh * Nq * D;
-  const size_t kv_off = (size_t)bh * Nk * D;
-  const rsrc_t rq = make_rsrc(q + head_off, (unsigned)Nq * (2 * D));
-  const rsrc_t rg = make_rsrc(dout + head_off, (unsigned)Nq * (2 * D));
+  const int chr = dr >> 3;  // 16-byte chunks of a row that hold data
+  const int ldq = 2 * mq.ld, ldg = 2 * mg.ld;  // row strides in bytes
+  const rsrc_t rq = make_rsrc(q + mq.head(bh, H), (unsigned)(Nq * ldq));
+  const rsrc_t rg = make_rsrc(dout + mg.head(bh, H), (unsigned)(Nq * ldg));
   const rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)Nq * 4);
   const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)Nq * 4);
 
   // held fragments (B operands, columns = this block's keys): K for role P, V for role dS
   const int key = kt * kDkvBK + kb * 32 + (lane & 31);
-  const rsrc_t rh = make_rsrc((role_p ? k : v) + kv_off, (unsigned)Nk * (2 * D));
+  const Map& mh = role_p ? mk : mv;
+  const int ldh = 2 * mh.ld;
+  const rsrc_t rh = make_rsrc((role_p ? k : v) + mh.head(bh, H), (unsigned)(Nk * ldh));
   bf16x8 hf[KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) hf[kk] = as_bf16x8(buffer_load16(rh, key * (2 * D) + 32 * kk + 16 * h));
+  for (int kk = 0; kk < KK; ++kk) hf[kk] = as_bf16x8(buffer_load16(rh, chunk_offset(key, 2 * kk + h, ldh, chr)));
 
-  TileDma<D, kDkvBQ, NWAVES> dma;
-  dma.init(wave, lane);
+  TileDma<D, kDkvBQ, NWAVES> dma, dmg;  // Q and dO tiles
+  dma.init(wave, lane, ldq, chr);
+  dmg.init(wave, lane, ldg, chr);
   RowFrag<D> rf;
   rf.init(lane);
   TrFrag<D> tf;
@@ -156,8 +171,8 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 
   auto issue_tile = [&](auto slot_tag, int t) {
     constexpr int SL = decltype(slot_tag)::value;
-    dma.issue(rq, t * kDkvBQ, qbuf[SL]);
-    dma.issue(rg, t * kDkvBQ, gbuf[SL]);
+    dma.issue(rq, t * kDkvBQ, ldq, qbuf[SL]);
+    dmg.issue(rg, t * kDkvBQ, ldg, gbuf[SL]);
     stats_dma(rd, rl, t * kDkvBQ, sbuf[SL], lane);
   };
 
@@ -165,13 +180,13 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // The row statistics (and role dS's P) of both query blocks are read
   // before `prefetch` requests the next tile, so that none of these LDS
   // reads has to wait for that DMA.
-  auto run_tile = [&](auto role_tag, auto slot_tag, auto&& prefetch) {
+  auto run_tile = [&](auto role_tag, auto slot_tag, int tile, auto&& prefetch) {
     constexpr bool RP = decltype(role_tag)::value;
     constexpr int SL = decltype(slot_tag)::value;
     const char* qs = qbuf[SL];
     const char* gs = gbuf[SL];
     const float* st = sbuf[SL];
-    uint4(*xb)[2][64] = xbuf[SL][kb];
+    uint4(*xb)[2][64] = xbuf[XR == RING ? SL : (tile & 1)][kb];
 
     f32x16 m1[2];          // S (P) or dP (dS), per query block
     bf16x8 ob[2][2];       // bf16 operands of P or dS [block][contraction step]
@@ -181,7 +196,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     // A operand of op i
     auto read_a = [&](int i) -> bf16x8 {
       const int ph = i / PH, j = i % PH, qb = ph & 1;
-      if (ph < 2) return lds_frag_row(RP ? qs : gs, qb * 32 * 2 * D + rf.off[j]);
+      if (ph < 2) return lds_frag_row(RP ? qs : gs, qb * 32 * 2 * D + rf.at(j));
       return tf.load(RP ? gs : qs, qb * 32 + 16 * (j / NCB), j % NCB);
     };
     auto read_side = [&](int qb) {
@@ -194,9 +209,12 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       }
     };
     auto valu = [&](int qb, int u) {
+      // rows u*16/PH .. (u+1)*16/PH - 1 (PH = 4 or 8: 16/PH rows per slot)
+      constexpr int RMAX = (16 + PH - 1) / PH;
 #pragma unroll
-      for (int rr = 0; rr < RPS; ++rr) {
-        const int r = u * RPS + rr;
+      for (int rr = 0; rr < RMAX; ++rr) {
+        const int r = (u * 16 + PH - 1) / PH + rr;
+        if (r >= ((u + 1) * 16 + PH - 1) / PH) break;
         const float sv = stat[qb][r >> 2][r & 3];
         float x;
         if constexpr (RP) {
@@ -256,10 +274,10 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     // tile t+1 past the end: zero rows, never read
     auto prefetch = [&]() { issue_tile(slot_next, t + 1); };
     if (role_p) {
-      if (do_p) run_tile(RoleP{}, slot_p, prefetch);
+      if (do_p) run_tile(RoleP{}, slot_p, t, prefetch);
       else prefetch();
     } else {
-      if (do_ds) run_tile(RoleDs{}, slot_ds, prefetch);
+      if (do_ds) run_tile(RoleDs{}, slot_ds, t - 1, prefetch);
       else prefetch();
     }
     wait_vmem();
@@ -275,18 +293,22 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     iteration(S0{}, S1{}, S2{}, t + 2, true, true);
   }
   // last: role dS on tile n_pad-1 (slot 0, since n_pad = 1 mod 3)
-  if (!role_p) run_tile(RoleDs{}, S0{}, [] {});
+  if (!role_p) run_tile(RoleDs{}, S0{}, n_pad - 1, [] {});
   (void)DMA_PER_TILE;
 
   if (key < Nk) {
-    float* out = (role_p ? dv : dk) + kv_off + (size_t)key * D;
+    const Map& mout = role_p ? mdv : mdk;
+    float* out = (role_p ? dv : dk) + mout.head(bh, H) + (size_t)key * mout.ld;
     const float f = role_p ? 1.f : scale;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
-        *reinterpret_cast<float4*>(out + 32 * cb + 8 * g + 4 * h) =
-            make_float4(acc[cb][4 * g] * f, acc[cb][4 * g + 1] * f, acc[cb][4 * g + 2] * f, acc[cb][4 * g + 3] * f);
+      for (int g = 0; g < 4; ++g) {
+        const int col = 32 * cb + 8 * g + 4 * h;  // d is a multiple of 8: four columns are all in or all out
+        if (col < dr)
+          *reinterpret_cast<float4*>(out + col) =
+              make_float4(acc[cb][4 * g] * f, acc[cb][4 * g + 1] * f, acc[cb][4 * g + 2] * f, acc[cb][4 * g + 3] * f);
+      }
   }
 }
 
@@ -308,13 +330,13 @@ template <int D, int NW>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
-    float* __restrict__ dq, int Nq, int Nk, int n_qtiles, int total, float c, float scale, int accumulate) {
+    float* __restrict__ dq, const Map mq, const Map mk, const Map mv, const Map mg, const Map mdq, int H, int dr,
+    int Nq, int Nk, int n_qtiles, int total, float c, float scale, int accumulate) {
   constexpr int BM = 32 * NW;
   constexpr int BN = 32;
   constexpr int KK = D / 16, NCB = D / 32;
   constexpr int NS = 2 * KK;       // S and dP ops per tile
   constexpr int NQ = KK;           // dQ ops per tile (2 contraction steps x NCB)
-  constexpr int RPS = 16 / NS > 0 ? 16 / NS : 1;
   constexpr int TILE_BYTES = BN * D * 2;
   constexpr int RING = 6;
   // One variable per ring slot (no wait for reads of one slot while the DMA
@@ -342,19 +364,19 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
 
   // queries, dO, dQ and the row statistics have Nq rows per (b, h); K and V have Nk
-  const size_t head_off = (size_t)bh * Nq * D;
-  const size_t kv_off = (size_t)bh * Nk * D;
-  const rsrc_t rq = make_rsrc(q + head_off, (unsigned)Nq * (2 * D));
-  const rsrc_t rg = make_rsrc(dout + head_off, (unsigned)Nq * (2 * D));
-  const rsrc_t rk = make_rsrc(k + kv_off, (unsigned)Nk * (2 * D));
-  const rsrc_t rv = make_rsrc(v + kv_off, (unsigned)Nk * (2 * D));
+  const int chr = dr >> 3;  // 16-byte chunks of a row that hold data
+  const int ldq = 2 * mq.ld, ldg = 2 * mg.ld, ldk = 2 * mk.ld, ldv = 2 * mv.ld;  // row strides in bytes
+  const rsrc_t rq = make_rsrc(q + mq.head(bh, H), (unsigned)(Nq * ldq));
+  const rsrc_t rg = make_rsrc(dout + mg.head(bh, H), (unsigned)(Nq * ldg));
+  const rsrc_t rk = make_rsrc(k + mk.head(bh, H), (unsigned)(Nk * ldk));
+  const rsrc_t rv = make_rsrc(v + mv.head(bh, H), (unsigned)(Nk * ldv));
 
   const int qrow = qt * BM + wave * 32 + (lane & 31);
   bf16x8 qf[KK], gf[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
-    qf[kk] = as_bf16x8(buffer_load16(rq, qrow * (2 * D) + 32 * kk + 16 * h));
-    gf[kk] = as_bf16x8(buffer_load16(rg, qrow * (2 * D) + 32 * kk + 16 * h));
+    qf[kk] = as_bf16x8(buffer_load16(rq, chunk_offset(qrow, 2 * kk + h, ldq, chr)));
+    gf[kk] = as_bf16x8(buffer_load16(rg, chunk_offset(qrow, 2 * kk + h, ldg, chr)));
   }
   const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)Nq * 4);
   const rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)Nq * 4);
@@ -362,8 +384,9 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   const float l2 = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, qrow * 4, 0, 0));
   const float dval = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, qrow * 4, 0, 0));
 
-  TileDma<D, BN, NW> dma;
-  dma.init(wave, lane);
+  TileDma<D, BN, NW> dma, dmv;  // K and V tiles
+  dma.init(wave, lane, ldk, chr);
+  dmv.init(wave, lane, ldv, chr);
   RowFrag<D> rf;
   rf.init(lane);
   TrFrag<D> tf;
@@ -377,8 +400,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   // prologue: tiles 0 .. 3 requested (tiles past the end read as zeros), scores of tile 0
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    dma.issue(rk, t * BN, kbuf[t]);
-    dma.issue(rv, t * BN, vbuf[t]);
+    dma.issue(rk, t * BN, ldk, kbuf[t]);
+    dmv.issue(rv, t * BN, ldv, vbuf[t]);
   }
   wait_vmem();
   __syncthreads();
@@ -386,7 +409,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
     if (i % KK == 0) sa[i / KK] = zero16();
-    sa[i / KK] = mfma32(lds_frag_row(i < KK ? kbuf[0] : vbuf[0], rf.off[i % KK]), i < KK ? qf[i] : gf[i - KK],
+    sa[i / KK] = mfma32(lds_frag_row(i < KK ? kbuf[0] : vbuf[0], rf.at(i % KK)), i < KK ? qf[i] : gf[i - KK],
                         sa[i / KK]);
   }
 
@@ -420,8 +443,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
       constexpr int W = NS + NCB - 1;
       static_assert(7 * W / 16 <= NS - 2 && 15 * W / 16 <= NS + NCB - 2, "dS ready before its dQ op");
       auto load_op = [&](int i) -> bf16x8 {
-        if (i < KK) return lds_frag_row(kbuf[NX], rf.off[i]);
-        if (i < NS) return lds_frag_row(vbuf[NX], rf.off[i - KK]);
+        if (i < KK) return lds_frag_row(kbuf[NX], rf.at(i));
+        if (i < NS) return lds_frag_row(vbuf[NX], rf.at(i - KK));
         const int t = i - NS;
         return tf.load(ks, 16 * (t / NCB), t % NCB);
       };
@@ -438,8 +461,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
           constexpr int t = i - NS;
           dqacc[t % NCB] = mfma32(aq[i & 1], dsb[t / NCB], dqacc[t % NCB]);
         }
-        if constexpr (i == 1) dma.issue(rk, (j + 4) * BN, kbuf[RF]);
-        if constexpr (i == 3) dma.issue(rv, (j + 4) * BN, vbuf[RF]);
+        if constexpr (i == 1) dma.issue(rk, (j + 4) * BN, ldk, kbuf[RF]);
+        if constexpr (i == 3) dmv.issue(rv, (j + 4) * BN, ldv, vbuf[RF]);
         static_for<0, 16>([&](auto RC) __attribute__((always_inline)) {
           constexpr int r = decltype(RC)::value;
           if constexpr (r * W / 16 == i) row(r);
@@ -495,12 +518,14 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   wait_vmem();  // requests past the last tile must land before this LDS is reassigned
 
   if (qrow < Nq) {
-    float* row = dq + head_off + (size_t)qrow * D;
+    float* row = dq + mdq.head(bh, H) + (size_t)qrow * mdq.ld;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        float4* dst = reinterpret_cast<float4*>(row + 32 * cb + 8 * g + 4 * h);
+        const int col = 32 * cb + 8 * g + 4 * h;  // d is a multiple of 8: four columns are all in or all out
+        if (col >= dr) continue;
+        float4* dst = reinterpret_cast<float4*>(row + col);
         float4 val = make_float4(dqacc[cb][4 * g] * scale, dqacc[cb][4 * g + 1] * scale,
                                  dqacc[cb][4 * g + 2] * scale, dqacc[cb][4 * g + 3] * scale);
         if (accumulate) {  // this call's dQ is one key segment's share
@@ -514,12 +539,12 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
 
 // ------------------------------------------------------------------ launch
 
-template <int D>
-static hipError_t rowdot_d(const BwdArgs& a) {
-  const long rows = (long)a.BH * a.Nq;
-  constexpr int rows_per_block = 256 / (D / 8);
-  hipLaunchKernelGGL(attn_bwd_rowdot_kernel<D>, dim3((unsigned)((rows + rows_per_block - 1) / rows_per_block)),
-                     dim3(256), 0, a.stream, a.dout, a.o, a.lse, a.drow, a.lse2, rows);
+template <int LPR>
+static hipError_t rowdot_l(const BwdArgs& a) {
+  const int rows = a.BH * a.Nq;
+  constexpr int rows_per_block = 256 / LPR;
+  hipLaunchKernelGGL(attn_bwd_rowdot_kernel<LPR>, dim3((unsigned)((rows + rows_per_block - 1) / rows_per_block)),
+                     dim3(256), 0, a.stream, a.dout, a.o, a.lse, a.drow, a.lse2, a.mg, a.mo, a.H, a.Nq, a.d, rows);
   return hipGetLastError();
 }
 
@@ -528,17 +553,21 @@ static hipError_t dkdv_d(const BwdArgs& a) {
   const int n_kt = (a.Nk + kDkvBK - 1) / kDkvBK;
   const int total = a.BH * n_kt;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(total), dim3(2 * kBwdThreads), 0, a.stream, a.q, a.k, a.v,
-                     a.dout, a.drow, a.lse2, a.dk, a.dv, a.Nq, a.Nk, n_kt, total, a.scale * kLog2e, a.scale);
+                     a.dout, a.drow, a.lse2, a.dk, a.dv, a.mq, a.mk, a.mv, a.mg, a.mdk, a.mdv, a.H, a.d, a.Nq, a.Nk,
+                     n_kt, total, a.scale * kLog2e, a.scale);
   return hipGetLastError();
 }
 
-#define VITATTN_DKDV_INSTANTIATE(D)                                                                         \
-  template __global__ void attn_bwd_dkdv_kernel<D>(                                                        \
-      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,            \
+#define VITATTN_DKDV_INSTANTIATE(D)                                                                            \
+  template __global__ void attn_bwd_dkdv_kernel<D>(                                                           \
+      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
-      float* __restrict__, int, int, int, int, float, float);
+      float* __restrict__, const Map, const Map, const Map, const Map, const Map, const Map, int, int, int, int, \
+      int, int, float, float);
 VITATTN_DKDV_INSTANTIATE(128)
 VITATTN_DKDV_INSTANTIATE(64)
+VITATTN_DKDV_INSTANTIATE(96)
+VITATTN_DKDV_INSTANTIATE(160)
 #undef VITATTN_DKDV_INSTANTIATE
 
 template <int D, int NW>
@@ -546,34 +575,56 @@ static hipError_t dq_v(const BwdArgs& a) {
   const int n_qt = (a.Nq + 32 * NW - 1) / (32 * NW);
   const int total = a.BH * n_qt;
   hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v, a.dout,
-                     a.drow, a.lse2, a.dq, a.Nq, a.Nk, n_qt, total, a.scale * kLog2e, a.scale,
-                     a.accumulate_dq ? 1 : 0);
+                     a.drow, a.lse2, a.dq, a.mq, a.mk, a.mv, a.mg, a.mdq, a.H, a.d, a.Nq, a.Nk, n_qt, total,
+                     a.scale * kLog2e, a.scale, a.accumulate_dq ? 1 : 0);
   return hipGetLastError();
 }
 
-#define VITATTN_DQ_INSTANTIATE(D, NW)                                                                       \
-  template __global__ void attn_bwd_dq_kernel<D, NW>(                                                      \
-      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,            \
+#define VITATTN_DQ_INSTANTIATE(D, NW)                                                                          \
+  template __global__ void attn_bwd_dq_kernel<D, NW>(                                                         \
+      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
-      int, int, int, int, float, float, int);
+      const Map, const Map, const Map, const Map, const Map, int, int, int, int, int, int, float, float, int);
 VITATTN_DQ_INSTANTIATE(128, 4)
 VITATTN_DQ_INSTANTIATE(128, 8)
 VITATTN_DQ_INSTANTIATE(64, 4)
 VITATTN_DQ_INSTANTIATE(64, 8)
+VITATTN_DQ_INSTANTIATE(96, 8)
+VITATTN_DQ_INSTANTIATE(160, 8)
 #undef VITATTN_DQ_INSTANTIATE
 
 template <int D>
 static hipError_t dq_d(const BwdArgs& a) {
-  switch (tuning_variant("VITATTN_DQ_VARIANT")) {
-    case 1: return dq_v<D, 4>(a);
-    case 2: return dq_v<D, 8>(a);
-    default: return dq_v<D, 8>(a);
+  if constexpr (D == 64 || D == 128) {
+    switch (tuning_variant("VITATTN_DQ_VARIANT")) {
+      case 1: return dq_v<D, 4>(a);
+      default: return dq_v<D, 8>(a);
+    }
+  } else {
+    return dq_v<D, 8>(a);
   }
 }
 
-hipError_t launch_bwd_rowdot(const BwdArgs& a) { return a.d == 128 ? rowdot_d<128>(a) : rowdot_d<64>(a); }
-hipError_t launch_bwd_dkdv(const BwdArgs& a) { return a.d == 128 ? dkdv_d<128>(a) : dkdv_d<64>(a); }
-hipError_t launch_bwd_dq(const BwdArgs& a) { return a.d == 128 ? dq_d<128>(a) : dq_d<64>(a); }
+hipError_t launch_bwd_rowdot(const BwdArgs& a) {
+  const int chunks = a.d / 8;
+  return chunks <= 8 ? rowdot_l<8>(a) : chunks <= 16 ? rowdot_l<16>(a) : rowdot_l<32>(a);
+}
+hipError_t launch_bwd_dkdv(const BwdArgs& a) {
+  switch (tile_width(a.d)) {
+    case 64: return dkdv_d<64>(a);
+    case 96: return dkdv_d<96>(a);
+    case 128: return dkdv_d<128>(a);
+    default: return dkdv_d<160>(a);
+  }
+}
+hipError_t launch_bwd_dq(const BwdArgs& a) {
+  switch (tile_width(a.d)) {
+    case 64: return dq_d<64>(a);
+    case 96: return dq_d<96>(a);
+    case 128: return dq_d<128>(a);
+    default: return dq_d<160>(a);
+  }
+}
 
 hipError_t launch_bwd(const BwdArgs& a) {
   hipError_t e = launch_bwd_rowdot(a);

@@ -14,10 +14,11 @@
 // gathered with ds_read_b64_tr_b16 from a row-major LDS tile in that same
 // row order (frag_tr below), so no tile is ever transposed in memory.
 //
-// LDS tiles are row-major [rows][d] bf16 with the 16-byte chunks of row r
+// LDS tiles are row-major [rows][D] bf16 with the 16-byte chunks of row r
 // XOR-swizzled by swz(r), so that both the row-fragment reads (32 rows x one
 // chunk) and the transposing reads (8 rows x 4 chunks) touch every bank
-// equally often.
+// equally often. The tile width D is 64, 96, 128 or 160; a head dim d below
+// D occupies the first d columns and the rest of each row holds zeros.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -51,46 +52,22 @@ __device__ __forceinline__ f32x16 zero16() {
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
 // Swizzled byte offset of 16-byte chunk c of row r in a [rows][D] bf16 tile.
+// D = 128 and 64: 16 consecutive rows of one chunk cover all 64 banks. D = 96
+// and 160 (rows of 192 and 320 bytes): four consecutive rows already start in
+// four different 64-byte bank groups, so the swizzle permutes chunks only
+// within their aligned group of four (never past the end of the row) and
+// varies with rows 4 apart.
 template <int D>
 __device__ __forceinline__ int swz(int r) {
+  static_assert(D == 64 || D == 96 || D == 128 || D == 160, "tile width");
   if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
-  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+  else if constexpr (D == 64) return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+  else return (r >> 2) & 3;
 }
 template <int D>
 __device__ __forceinline__ int tile_off(int r, int c) {
   return r * (2 * D) + 16 * (c ^ swz<D>(r));
 }
-
-// Global -> registers: a tile of R rows x D bf16 starting at row0 of a
-// contiguous [N][D] matrix; rows at or past N read as zeros.
-template <int D, int R, int NT>
-struct TileLoader {
-  static constexpr int CH = D / 8;                 // 16-byte chunks per row
-  static constexpr int PER_THREAD = R * CH / NT;   // chunks per thread
-  static_assert(R * CH % NT == 0, "tile must divide evenly among threads");
-  uint4 r[PER_THREAD];
-
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ base, int row0, int N, int tid) {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int id = tid + i * NT;
-      const int row = row0 + id / CH;
-      const int c = id % CH;
-      if (row < N) {
-        r[i] = *reinterpret_cast<const uint4*>(base + (size_t)row * D + c * 8);
-      } else {
-        r[i] = make_uint4(0, 0, 0, 0);
-      }
-    }
-  }
-  __device__ __forceinline__ void store(char* lds, int tid) const {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int id = tid + i * NT;
-      *reinterpret_cast<uint4*>(lds + tile_off<D>(id / CH, id % CH)) = r[i];
-    }
-  }
-};
 
 // Row fragment: lane l gets T[r0 + l%32][16*kk + 8*(l/32) .. +7] (an A or B
 // operand whose contraction runs along d). `roff` is the lane's precomputed
@@ -99,26 +76,27 @@ __device__ __forceinline__ bf16x8 lds_frag_row(const char* lds, int off) {
   return as_bf16x8(*reinterpret_cast<const uint4*>(lds + off));
 }
 
+// Tile widths whose swizzle permutes chunks within aligned groups of four:
+// moving a fragment by one group (64 bytes) is then a plain constant offset.
+template <int D>
+constexpr bool kGrouped = (D == 96 || D == 160);
+
 // Per-lane offsets of the row fragments of rows r0 + l%32 (r0 a multiple of
-// 32, added by the caller as r0 * 2D), for every kk = 0 .. D/16 - 1.
+// 32, added by the caller as r0 * 2D), for every kk = 0 .. D/16 - 1. For the
+// grouped widths chunk 2*kk + h sits in group kk/2 at position 2*(kk%2) + h,
+// so two registers cover every kk.
 template <int D>
 struct RowFrag {
-  int off[D / 16];
+  int off_[kGrouped<D> ? 2 : D / 16];
   __device__ __forceinline__ void init(int lane) {
     const int row = lane & 31, h = lane >> 5;
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) off[kk] = tile_off<D>(row, 2 * kk + h);
+    for (int kk = 0; kk < (kGrouped<D> ? 2 : D / 16); ++kk) off_[kk] = tile_off<D>(row, 2 * kk + h);
   }
-};
-
-// Same offsets from one register: chunk 2*kk + h of a row swizzled by s is
-// 2*kk ^ (h ^ s) (2*kk is even and h < 2), and the row term only has bits
-// above the chunk bits, so the offset of step kk is base ^ (32 * kk).
-template <int D>
-struct RowFragX {
-  int base;
-  __device__ __forceinline__ void init(int lane) { base = tile_off<D>(lane & 31, lane >> 5); }
-  __device__ __forceinline__ int off(int kk) const { return base ^ (32 * kk); }
+  __device__ __forceinline__ int at(int kk) const {
+    if constexpr (kGrouped<D>) return off_[kk & 1] + 64 * (kk >> 1);
+    else return off_[kk];
+  }
 };
 
 // Transposed fragment: operand whose contraction runs along rows. For
@@ -127,17 +105,19 @@ struct RowFragX {
 // in slot t = 0..7 — the row order of an accumulator reused as an operand.
 // Built from two ds_read_b64_tr_b16: within each 16-lane group, lane i of the
 // result takes element i%4 of the 8 bytes addressed by lane 4e + i/4 of the
-// group, for e = 0..3.
+// group, for e = 0..3. A column block is one chunk group, so for the grouped
+// widths block cb is block 0 plus 64*cb bytes.
 template <int D>
 struct TrFrag {
-  int off[2][D / 32];  // [read][column block]
+  static constexpr int NCB = kGrouped<D> ? 1 : D / 32;
+  int off[2][NCB];  // [read][column block]
   __device__ __forceinline__ void init(int lane) {
     const int g = lane >> 4, j = lane & 15;
 #pragma unroll
     for (int rd = 0; rd < 2; ++rd) {
       const int row = 8 * rd + 4 * (g >> 1) + (j >> 2);
 #pragma unroll
-      for (int cb = 0; cb < D / 32; ++cb) {
+      for (int cb = 0; cb < NCB; ++cb) {
         const int col = 32 * cb + 16 * (g & 1) + 4 * (j & 3);
         off[rd][cb] = row * (2 * D) + 16 * ((col >> 3) ^ swz<D>(row)) + 2 * (col & 7);
       }
@@ -146,32 +126,10 @@ struct TrFrag {
   // k0: contraction base row (multiple of 16); the row part of the swizzle
   // depends only on the low 4 row bits, so k0 enters as a plain offset.
   __device__ __forceinline__ bf16x8 load(const char* lds, int k0, int cb) const {
-    const char* p0 = lds + k0 * (2 * D) + off[0][cb];
-    const char* p1 = lds + k0 * (2 * D) + off[1][cb];
-    bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
-    bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p1));
-    bf16x8 r;
-    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
-    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
-    return r;
-  }
-};
-
-// TrFrag with two offset registers: column block cb moves the chunk index
-// by 4*cb, which lies in chunk bits the row swizzle XORs but no other term
-// of the offset touches, so the offset for cb is off[read] ^ (64 * cb).
-template <int D>
-struct TrFragX {
-  int off[2];
-  __device__ __forceinline__ void init(int lane) {
-    TrFrag<D> t;
-    t.init(lane);
-    off[0] = t.off[0][0];
-    off[1] = t.off[1][0];
-  }
-  __device__ __forceinline__ bf16x8 load(const char* lds, int k0, int cb) const {
-    const char* p0 = lds + k0 * (2 * D) + (off[0] ^ (64 * cb));
-    const char* p1 = lds + k0 * (2 * D) + (off[1] ^ (64 * cb));
+    const int o0 = kGrouped<D> ? off[0][0] + 64 * cb : off[0][cb];
+    const int o1 = kGrouped<D> ? off[1][0] + 64 * cb : off[1][cb];
+    const char* p0 = lds + k0 * (2 * D) + o0;
+    const char* p1 = lds + k0 * (2 * D) + o1;
     bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
     bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p1));
     bf16x8 r;
@@ -227,46 +185,72 @@ __device__ __forceinline__ uint4 buffer_load16(rsrc_t r, int byte_off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
 }
 
+// Byte offset that lies past every buffer the kernels build (their sizes stay
+// below 2^31), so a load from it returns zeros: used for the columns of a
+// tile beyond the head dim.
+constexpr unsigned kOobOffset = 0x80000000u;
+
+// Byte offset of 16-byte chunk `chunk` of row `row` of a bf16 matrix whose
+// rows are ld_bytes apart and hold chr real chunks; chunks past the head dim
+// point past the buffer and read as zeros.
+__device__ __forceinline__ int chunk_offset(int row, int chunk, int ld_bytes, int chr) {
+  return chunk < chr ? row * ld_bytes + 16 * chunk : (int)kOobOffset;
+}
+
 // Direct global -> LDS copy of an R x D bf16 tile (rows row0 .. row0+R-1 of
-// a [N][D] matrix behind `r`) into the swizzled layout of tile_off. One
-// wave instruction fills 1 KB of consecutive LDS (16 bytes per lane), so
-// each lane fetches the chunk whose swizzled home is its LDS slot. Rows past
-// the end read as zeros. The NW waves of the group split the instructions.
+// a matrix behind `r` whose rows are ld_bytes apart and hold chr real 16-byte
+// chunks) into the swizzled layout of tile_off. One wave instruction fills
+// 1 KB of consecutive LDS (16 bytes per lane), so each lane fetches the chunk
+// whose swizzled home is its LDS slot. Rows past the end and chunks past the
+// head dim read as zeros. The NW waves of the group split the instructions;
+// every wave issues the same number per tile (PER_WAVE), so that one vmcnt
+// bound fits all of them: when the instruction count is not a multiple of NW
+// the surplus slots repeat other waves' instructions (the same bytes into the
+// same LDS slot), and with fewer instructions than waves the waves without
+// one issue nothing.
 template <int D, int R, int NW>
 struct TileDma {
   static constexpr int CH = D / 8;
+  static_assert(R * CH % 64 == 0, "a tile is a whole number of 1 KB wave instructions");
   static constexpr int INSTR = R * CH / 64;  // wave instructions per tile
-  static constexpr int PER_WAVE = INSTR >= NW ? INSTR / NW : 1;
-  static_assert(INSTR % NW == 0 || NW % INSTR == 0, "tile must divide evenly among waves");
   static constexpr bool ALL_ACTIVE = INSTR >= NW;  // every wave has a share
-  int voff[PER_WAVE];  // byte offset of this lane's chunk relative to row0
-  int lds_off;         // LDS byte offset of this wave's first instruction
-  bool active;         // false for waves left without work on small tiles
+  static constexpr bool BLOCKED = INSTR % NW == 0 || !ALL_ACTIVE;  // contiguous instructions per wave
+  static constexpr int PER_WAVE = ALL_ACTIVE ? (INSTR + NW - 1) / NW : 1;
+  unsigned voff[PER_WAVE];  // byte offset of this lane's chunk relative to row0
+  int lds_off[BLOCKED ? 1 : PER_WAVE];  // LDS byte offset of this wave's (first) instruction
+  bool active;              // false for waves left without work on small tiles
 
-  __device__ __forceinline__ void init(int wave, int lane) {
+  __device__ __forceinline__ static int instr(int wave, int i) {
+    if constexpr (BLOCKED) return (wave * PER_WAVE + i) % INSTR;
+    else return (wave + NW * i) % INSTR;
+  }
+  __device__ __forceinline__ void init(int wave, int lane, int ld_bytes, int chr) {
 #pragma unroll
     for (int i = 0; i < PER_WAVE; ++i) {
-      const int gi = (wave * PER_WAVE + i) % INSTR;
+      const int gi = instr(wave, i);
       const int pos = gi * 64 + lane;  // 16-byte slot in the tile
-      const int row = pos / CH, pc = pos % CH;
-      voff[i] = row * (2 * D) + 16 * (pc ^ swz<D>(row));
+      const int row = pos / CH, pc = (pos % CH) ^ swz<D>(row);
+      voff[i] = (unsigned)chunk_offset(row, pc, ld_bytes, chr);
+      if constexpr (!BLOCKED) lds_off[i] = gi * 1024;
     }
-    lds_off = (wave * PER_WAVE) % INSTR * 1024;
+    if constexpr (BLOCKED) lds_off[0] = instr(wave, 0) * 1024;
     active = wave * PER_WAVE < INSTR;
   }
-  // Instruction i (< PER_WAVE) of this wave's share of the tile.
-  __device__ __forceinline__ void issue_one(rsrc_t r, int row0, char* lds_tile, int i) const {
-    if (!ALL_ACTIVE && !active) return;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(lds_tile + lds_off + i * 1024), 16,
-                                             row0 * (2 * D) + voff[i], 0, 0, 0);
+  __device__ __forceinline__ char* lds_slot(char* lds_tile, int i) const {
+    if constexpr (BLOCKED) return lds_tile + lds_off[0] + i * 1024;
+    else return lds_tile + lds_off[i];
   }
-  __device__ __forceinline__ void issue(rsrc_t r, int row0, char* lds_tile) const {
+  // Instruction i (< PER_WAVE) of this wave's share of the tile; row0 *
+  // ld_bytes stays below 2^31, so adding an out-of-range chunk offset cannot
+  // wrap around into the buffer.
+  __device__ __forceinline__ void issue_one(rsrc_t r, int row0, int ld_bytes, char* lds_tile, int i) const {
     if (!ALL_ACTIVE && !active) return;
-    const int base = row0 * (2 * D);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_slot(lds_tile, i), 16,
+                                             (int)((unsigned)(row0 * ld_bytes) + voff[i]), 0, 0, 0);
+  }
+  __device__ __forceinline__ void issue(rsrc_t r, int row0, int ld_bytes, char* lds_tile) const {
 #pragma unroll
-    for (int i = 0; i < PER_WAVE; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(lds_tile + lds_off + i * 1024), 16, base + voff[i], 0,
-                                               0, 0);
+    for (int i = 0; i < PER_WAVE; ++i) issue_one(r, row0, ld_bytes, lds_tile, i);
   }
 };
 

@@ -12,6 +12,11 @@
 //   P^T = exp2(S^T * scale*log2e - m)
 //   O^T (d x queries) += V^T P^T   -> P^T is reused in place as the operand
 //
+// Operands may have any batch / head / row strides (rows 16-byte aligned): the
+// kernel only forms addresses from them. The tile width D is 64, 96, 128 or
+// 160; for a head dim d below D the columns past d are loaded as zeros (they
+// add nothing to the scores) and never stored.
+//
 // Software pipeline across tiles: the scores of tile j+1 are computed on the
 // matrix cores while the vector units turn tile j's scores into
 // probabilities. K therefore runs one tile ahead of V, in two LDS rings of
@@ -50,19 +55,28 @@ constexpr bool exp_schedule_ok(int NS, int CPB, int KB, int W) {
   return true;
 }
 
+// Widest exponential window (at most NOPS - 5 slots, which leaves the last
+// slots to the row max of the next tile) that keeps exp_schedule_ok.
+constexpr int exp_window(int NS, int CPB, int KB, int NOPS) {
+  int w = NOPS - 5;
+  while (w > 1 && !exp_schedule_ok(NS, CPB, KB, w)) --w;
+  return w;
+}
+
 template <int D, int KB, int NW, int MINW>
 __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t* __restrict__ q,
                                                                  const uint16_t* __restrict__ k,
                                                                  const uint16_t* __restrict__ v,
                                                                  float* __restrict__ o, float* __restrict__ lse,
-                                                                 int Nq, int Nk, int n_qtiles, int total, float c) {
+                                                                 const Map mq, const Map mk, const Map mv,
+                                                                 const Map mo, int H, int dr, int Nq, int Nk,
+                                                                 int n_qtiles, int total, float c) {
   constexpr int BM = 32 * NW;  // query rows per workgroup
   constexpr int BN = 32 * KB;  // keys per tile
   constexpr int TILE_BYTES = BN * D * 2;
   constexpr int KK = D / 16;           // contraction steps of one 32-key score block
   constexpr int NS = KB * KK;          // score ops per tile
   constexpr int NV = 2 * KB * D / 32;  // PV ops per tile
-  constexpr int NPAIR = 8 * KB;        // score pairs per lane per tile
   // One variable per ring slot: the compiler then knows that reading one
   // slot never overlaps the DMA into another and inserts no wait for it.
   __shared__ __attribute__((aligned(1024))) char kbuf0[TILE_BYTES];
@@ -79,20 +93,21 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
 
   // queries (and O, LSE) have Nq rows per (b, h), keys and values Nk
-  const size_t head_off = (size_t)bh * Nq * D;
-  const size_t kv_off = (size_t)bh * Nk * D;
-  const rsrc_t rq = make_rsrc(q + head_off, (unsigned)Nq * (2 * D));
-  const rsrc_t rk = make_rsrc(k + kv_off, (unsigned)Nk * (2 * D));
-  const rsrc_t rv = make_rsrc(v + kv_off, (unsigned)Nk * (2 * D));
+  const int chr = dr >> 3;  // 16-byte chunks of a row that hold data
+  const int ldq = 2 * mq.ld, ldk = 2 * mk.ld, ldv = 2 * mv.ld;  // row strides in bytes
+  const rsrc_t rq = make_rsrc(q + mq.head(bh, H), (unsigned)(Nq * ldq));
+  const rsrc_t rk = make_rsrc(k + mk.head(bh, H), (unsigned)(Nk * ldk));
+  const rsrc_t rv = make_rsrc(v + mv.head(bh, H), (unsigned)(Nk * ldv));
 
   // Q fragments of this wave's 32 query rows (B operands of K Q^T)
   const int qrow = qt * BM + wave * 32 + (lane & 31);
   bf16x8 qf[KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) qf[kk] = as_bf16x8(buffer_load16(rq, qrow * (2 * D) + 32 * kk + 16 * h));
+  for (int kk = 0; kk < KK; ++kk) qf[kk] = as_bf16x8(buffer_load16(rq, chunk_offset(qrow, 2 * kk + h, ldq, chr)));
 
-  TileDma<D, BN, NW> dma;
-  dma.init(wave, lane);
+  TileDma<D, BN, NW> dma, dmv;  // K and V tiles (the two may have different row strides)
+  dma.init(wave, lane, ldk, chr);
+  dmv.init(wave, lane, ldv, chr);
   RowFrag<D> kfrag;
   kfrag.init(lane);
   TrFrag<D> vfrag;
@@ -105,9 +120,9 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   float l_part = 0.f;       // this lane's share of the sum of the bf16 probabilities
 
   const int n_kt = (Nk + BN - 1) / BN;
-  dma.issue(rk, 0, kbuf[0]);
-  dma.issue(rv, 0, vbuf[0]);
-  dma.issue(rk, BN, kbuf[1]);
+  dma.issue(rk, 0, ldk, kbuf[0]);
+  dmv.issue(rv, 0, ldv, vbuf[0]);
+  dma.issue(rk, BN, ldk, kbuf[1]);
   wait_vmem();
   __syncthreads();
 
@@ -146,7 +161,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
     if (i % KK == 0) sa[i / KK] = zero16();
-    sa[i / KK] = mfma32(lds_frag_row(kbuf[0], (i / KK) * 32 * 2 * D + kfrag.off[i % KK]), qf[i % KK], sa[i / KK]);
+    sa[i / KK] = mfma32(lds_frag_row(kbuf[0], (i / KK) * 32 * 2 * D + kfrag.at(i % KK)), qf[i % KK], sa[i / KK]);
   }
   if (n_kt == 1) mask_ragged(sa, 0);
   max_finish(fmaxf(fmaxf(max_quarter(sa, 0), max_quarter(sa, 1)), fmaxf(max_quarter(sa, 2), max_quarter(sa, 3))));
@@ -196,14 +211,14 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
 
     if constexpr (NEXT) {
       constexpr int NOPS = NS + NV;
-      constexpr int W = NOPS - 5;  // exponentials in slots 0 .. W-1
+      constexpr int W = exp_window(NS, CPB, KB, NOPS);  // exponentials in slots 0 .. W-1
       static_assert(exp_schedule_ok(NS, CPB, KB, W), "probabilities must be ready before their PV op");
       constexpr int NDMA = 2 * decltype(dma)::PER_WAVE;
       static_assert(2 * NDMA - 1 < NOPS, "DMA requests must fit the stream");
       // score op i: key block i % KB, contraction step i / KB (the KB
       // accumulator chains are interleaved, so consecutive ops are independent)
       auto load_op = [&](int i) -> bf16x8 {
-        if (i < NS) return lds_frag_row(ks, (i % KB) * 32 * 2 * D + kfrag.off[i / KB]);
+        if (i < NS) return lds_frag_row(ks, (i % KB) * 32 * 2 * D + kfrag.at(i / KB));
         const int t = i - NS;
         return vfrag.load(vs, 16 * (t / CPB), t % CPB);
       };
@@ -225,9 +240,9 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
         if constexpr ((i & 1) == 1 && i / 2 < NDMA) {
           constexpr int q = i / 2, PW = NDMA / 2;
           if constexpr (q < PW)
-            dma.issue_one(rk, (j + 2) * BN, kbuf[P], q);
+            dma.issue_one(rk, (j + 2) * BN, ldk, kbuf[P], q);
           else
-            dma.issue_one(rv, (j + 1) * BN, vbuf[1 - P], q - PW);
+            dmv.issue_one(rv, (j + 1) * BN, ldv, vbuf[1 - P], q - PW);
         }
         exp_slice(IC, std::integral_constant<int, W>{});
         if constexpr (i >= W && i < W + 4) {
@@ -283,14 +298,15 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   const float l = sum_halves(l_part);
   if (qrow < Nq) {
     const float inv = 1.0f / l;
-    float* orow = o + head_off + (size_t)qrow * D;
+    float* orow = o + mo.head(bh, H) + (size_t)qrow * mo.ld;
 #pragma unroll
     for (int cb = 0; cb < D / 32; ++cb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        const int col = 32 * cb + 8 * g + 4 * h;  // d is a multiple of 8: four columns are all in or all out
         float4 val = make_float4(oacc[cb][4 * g] * inv, oacc[cb][4 * g + 1] * inv, oacc[cb][4 * g + 2] * inv,
                                  oacc[cb][4 * g + 3] * inv);
-        *reinterpret_cast<float4*>(orow + 32 * cb + 8 * g + 4 * h) = val;
+        if (col < dr) *reinterpret_cast<float4*>(orow + col) = val;
       }
     if (h == 0) lse[(size_t)bh * Nq + qrow] = (m_run + __log2f(l)) * kLn2;
   }
@@ -303,21 +319,21 @@ static hipError_t launch_fwd_v(const FwdArgs& a) {
   const int total = a.BH * n_qtiles;
   const float c = a.scale * kLog2e;
   hipLaunchKernelGGL((attn_fwd_kernel<D, KB, NW, MINW>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v,
-                     a.o, a.lse, a.Nq, a.Nk, n_qtiles, total, c);
+                     a.o, a.lse, a.mq, a.mk, a.mv, a.mo, a.H, a.d, a.Nq, a.Nk, n_qtiles, total, c);
   return hipGetLastError();
 }
 
 // Every tile variant is instantiated explicitly: hipcc otherwise omits the
 // host-side launch stub of some instantiations reached only through this
 // dispatch, and the library then fails to load.
-#define VITATTN_FWD_VARIANTS(X) \
-  X(128, 2, 8, 2) X(128, 2, 4, 2) X(128, 1, 8, 2) X(64, 2, 8, 2) X(64, 2, 4, 2) X(64, 1, 8, 2)
-#define VITATTN_FWD_INSTANTIATE(D, KB, NW, MINW)                                                         \
-  template __global__ void attn_fwd_kernel<D, KB, NW, MINW>(const uint16_t* __restrict__,               \
-                                                            const uint16_t* __restrict__,               \
-                                                            const uint16_t* __restrict__,               \
-                                                            float* __restrict__, float* __restrict__, int, \
-                                                            int, int, int, float);
+#define VITATTN_FWD_VARIANTS(X)                                                                     \
+  X(128, 2, 8, 2) X(128, 2, 4, 2) X(128, 1, 8, 2) X(64, 2, 8, 2) X(64, 2, 4, 2) X(64, 1, 8, 2) X(96, 2, 8, 2) \
+      X(160, 1, 8, 2)
+#define VITATTN_FWD_INSTANTIATE(D, KB, NW, MINW)                                                               \
+  template __global__ void attn_fwd_kernel<D, KB, NW, MINW>(                                                  \
+      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
+      float* __restrict__, float* __restrict__, const Map, const Map, const Map, const Map, int, int, int, int, \
+      int, int, float);
 VITATTN_FWD_VARIANTS(VITATTN_FWD_INSTANTIATE)
 #undef VITATTN_FWD_INSTANTIATE
 
@@ -335,7 +351,12 @@ static hipError_t launch_fwd_d(const FwdArgs& a, int variant) {
 
 hipError_t launch_fwd(const FwdArgs& a) {
   const int variant = tuning_variant("VITATTN_FWD_VARIANT");
-  return a.d == 128 ? launch_fwd_d<128>(a, variant) : launch_fwd_d<64>(a, variant);
+  switch (tile_width(a.d)) {
+    case 64: return launch_fwd_d<64>(a, variant);
+    case 96: return launch_fwd_v<96, 2, 8, 2>(a);
+    case 128: return launch_fwd_d<128>(a, variant);
+    default: return launch_fwd_v<160, 1, 8, 2>(a);
+  }
 }
 
 }  // namespace vitattn

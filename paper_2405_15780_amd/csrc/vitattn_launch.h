@@ -6,13 +6,27 @@
 
 namespace vitattn {
 
+// Where the rows of one [B][H][N][d] operand live: element strides of the
+// batch, head and row dimensions (the d elements of a row are contiguous).
+struct Map {
+  long long sb, sh;
+  int ld;
+  __host__ __device__ long long head(int bh, int H) const { return (bh / H) * sb + (bh % H) * sh; }
+};
+inline Map dense_map(int H, int N, int d) { return Map{(long long)H * N * d, (long long)N * d, d}; }
+
+// Tile width of the attention kernels for head dim d (a multiple of 8, at
+// most 160): columns d .. D-1 of every tile are zeros.
+inline int tile_width(int d) { return d <= 64 ? 64 : d <= 96 ? 96 : d <= 128 ? 128 : 160; }
+
 struct FwdArgs {
   const uint16_t* q;
   const uint16_t* k;
   const uint16_t* v;
   float* o;
-  float* lse;
-  int BH, Nq, Nk, d;  // query rows and key rows per (b, h)
+  float* lse;  // [B][H][Nq], dense
+  Map mq, mk, mv, mo;
+  int H, BH, Nq, Nk, d;  // query rows and key rows per (b, h); d the head dim
   float scale;
   hipStream_t stream;
 };
@@ -23,13 +37,14 @@ struct BwdArgs {
   const uint16_t* v;
   const float* o;
   const uint16_t* dout;
-  const float* lse;
+  const float* lse;  // [B][H][Nq], dense
   float* dq;
   float* dk;
   float* dv;
   float* drow;  // workspace region 0: D = rowsum(dO o O), [BH][Nq]
   float* lse2;  // workspace region 1: LSE * log2(e), [BH][Nq]
-  int BH, Nq, Nk, d;  // query rows and key rows per (b, h)
+  Map mq, mk, mv, mo, mg, mdq, mdk, mdv;  // mg: dout
+  int H, BH, Nq, Nk, d;  // query rows and key rows per (b, h); d the head dim
   float scale;
   bool accumulate_dq;  // dq += this call's dQ instead of dq = ...
   hipStream_t stream;

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_status_strings_and_version():
-    assert va.version() == "0.2.0"
+    assert va.version() == "0.3.0"
     for s in range(6):
         assert va.status_str(s).startswith("VITATTN")
     assert "unknown" in va.status_str(99)
@@ -50,7 +50,9 @@ def test_workspace_bytes():
     assert va.workspace_bytes(1, 1, 8388351, 128) > 0
     assert va.workspace_bytes(1, 1, 8388352, 128) == 0
     assert va.workspace_bytes(1, 1, 0, 64) == 0
-    assert va.workspace_bytes(1, 1, 10, 96) == 0
+    assert va.workspace_bytes(1, 1, 10, 100) == 0
+    assert va.workspace_bytes(1, 1, 10, 168) == 0
+    assert va.workspace_bytes(1, 1, 10, 72) == 512
 
 
 class Bufs:
@@ -82,7 +84,8 @@ def fwd(b, B=1, H=1, N=8, d=64, scale=0.125, override=None):
 
 @pytest.mark.parametrize("kw,expected", [
     (dict(B=0), E_INVAL), (dict(H=0), E_INVAL), (dict(N=0), E_INVAL), (dict(N=-5), E_INVAL),
-    (dict(d=96), E_UNSUP), (dict(d=32), E_UNSUP), (dict(d=256), E_UNSUP),
+    (dict(d=100), E_UNSUP), (dict(d=4), E_UNSUP), (dict(d=0), E_UNSUP), (dict(d=168), E_UNSUP),
+    (dict(d=256), E_UNSUP),
     (dict(scale=float("nan")), E_INVAL), (dict(scale=float("inf")), E_INVAL), (dict(scale=0.0), E_INVAL),
     (dict(scale=-0.125), E_INVAL), (dict(B=65536, H=65536, N=2), E_INVAL),
 ])
@@ -115,7 +118,7 @@ def bwd(b, B=1, H=1, N=8, d=64, scale=0.125, ws_bytes=None, override=None):
 
 
 @pytest.mark.parametrize("kw,expected", [
-    (dict(N=0), E_INVAL), (dict(d=80), E_UNSUP), (dict(scale=float("nan")), E_INVAL),
+    (dict(N=0), E_INVAL), (dict(d=84), E_UNSUP), (dict(scale=float("nan")), E_INVAL),
     (dict(ws_bytes=31), E_WS), (dict(ws_bytes=0), E_WS), (dict(override={9: None}), E_WS),
     (dict(override={9: 12345}), E_WS),
 ])
@@ -160,7 +163,7 @@ def fwd_kv(b, B=1, H=1, Nq=8, Nk=5, d=64, scale=0.125, override=None):
 
 
 @pytest.mark.parametrize("kw,expected", [
-    (dict(Nk=0), E_INVAL), (dict(Nq=0), E_INVAL), (dict(Nk=-1), E_INVAL), (dict(d=72), E_UNSUP),
+    (dict(Nk=0), E_INVAL), (dict(Nq=0), E_INVAL), (dict(Nk=-1), E_INVAL), (dict(d=76), E_UNSUP),
     (dict(Nk=8388352, d=128), E_INVAL), (dict(scale=float("nan")), E_INVAL),
     (dict(override={1: None}), E_INVAL), (dict(override={2: 4100}), E_INVAL),
 ])
@@ -180,7 +183,7 @@ def bwd_kv(b, B=1, H=1, Nq=8, Nk=5, d=64, scale=0.125, flags=0, ws_bytes=None, o
 
 
 @pytest.mark.parametrize("kw,expected", [
-    (dict(Nk=0), E_INVAL), (dict(flags=2), E_INVAL), (dict(flags=-1), E_INVAL), (dict(d=160), E_UNSUP),
+    (dict(Nk=0), E_INVAL), (dict(flags=2), E_INVAL), (dict(flags=-1), E_INVAL), (dict(d=168), E_UNSUP),
     (dict(ws_bytes=1), E_WS), (dict(override={6: None}), E_INVAL), (dict(override={7: 4102}), E_INVAL),
 ])
 def test_bwd_kv_rejects_bad_arguments(kw, expected):
@@ -275,3 +278,64 @@ def test_product_package_does_not_import_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"^\s*(from|import)\s+oracle\b", text, flags=re.M), f
                 assert "oracle/" not in text, f
+
+
+# ------------------------------------------------------------ strided entry points
+
+
+def S(batch, head, row):
+    return va.Strides(batch, head, row)
+
+
+def fwd_strided(b, sq=None, sk=None, sv=None, so=None, B=2, H=2, Nq=8, Nk=8, d=72, scale=0.125):
+    dq = S(H * Nq * d, Nq * d, d)
+    dk = S(H * Nk * d, Nk * d, d)
+    return lib().vitattn_fwd_strided(b.p(0), sq or dq, b.p(1), sk or dk, b.p(2), sv or dk, b.p(3), so or dq, b.p(4),
+                                     B, H, Nq, Nk, d, scale, None)
+
+
+@pytest.mark.parametrize("kw,expected", [
+    (dict(sq=S(0, 0, 64)), E_INVAL),                  # row stride below d
+    (dict(sk=S(-8, 72, 144)), E_INVAL),               # negative stride
+    (dict(sv=S(1152, 576, 76)), E_INVAL),             # bf16 row stride not a multiple of 8
+    (dict(sq=S(1152, 572, 72)), E_INVAL),             # head stride misaligned
+    (dict(so=S(1152, 576, 74)), E_INVAL),             # fp32 row stride not a multiple of 4
+    (dict(so=S(576, 576, 72)), E_INVAL),              # output heads overlap batches
+    (dict(so=S(1152, 72, 72)), E_INVAL),              # output heads overlap rows
+    (dict(so=S(0, 576, 72)), E_INVAL),                # output batches repeat
+    (dict(sq=S(0, 0, 1 << 27)), E_INVAL),             # (rows + 256) * row bytes past 2^31
+    (dict(d=100), E_UNSUP), (dict(d=168), E_UNSUP), (dict(B=0), E_INVAL), (dict(scale=0.0), E_INVAL),
+])
+def test_fwd_strided_rejects_bad_layouts(kw, expected):
+    b = Bufs()
+    assert fwd_strided(b, **kw) == expected
+    assert b.untouched()
+
+
+def bwd_strided(b, bad=None, B=2, H=2, N=8, d=72, flags=0, ws_bytes=None):
+    dense = S(H * N * d, N * d, d)
+    st = [dense] * 8  # q k v o dout dq dk dv
+    if bad:
+        i, val = bad
+        st[i] = val
+    wsb = va.workspace_bytes(B, H, N, d) if ws_bytes is None else ws_bytes
+    return lib().vitattn_bwd_strided(b.p(0), st[0], b.p(1), st[1], b.p(2), st[2], b.p(3), st[3], b.p(4), st[4],
+                                     b.p(5), b.p(6), st[5], b.p(7), st[6], b.p(8), st[7], B, H, N, N, d, 0.125, flags,
+                                     b.p(9), wsb, None)
+
+
+@pytest.mark.parametrize("which", range(8))
+def test_bwd_strided_rejects_a_bad_layout_on_any_operand(which):
+    b = Bufs()
+    assert bwd_strided(b, bad=(which, S(1152, 576, 64))) == E_INVAL  # row stride below d
+    assert bwd_strided(b, bad=(which, S(1152, 576, 76 if which in (0, 1, 2, 4) else 74))) == E_INVAL
+    assert b.untouched()
+
+
+def test_bwd_strided_output_overlap_and_workspace():
+    b = Bufs()
+    for i in (5, 6, 7):  # dq, dk, dv may not overlap themselves
+        assert bwd_strided(b, bad=(i, S(576, 0, 72))) == E_INVAL
+    assert bwd_strided(b, flags=4) == E_INVAL
+    assert bwd_strided(b, ws_bytes=16) == E_WS
+    assert b.untouched()
