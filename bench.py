@@ -42,14 +42,18 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 512 MiB device copy (to scale rocprofv3 FETCH_SIZE/WRITE_SIZE)")
-    p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg"], default="attention",
-                   help="which kernel family to time (default: the attention forward+backward hot path)")
+    p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg", "d72", "d160", "bnhd"],
+                   default="attention",
+                   help="which workload to time (default: the attention forward+backward hot path at "
+                        "N=188,416, d=128; d72 / d160: the paper's other head dims; bnhd: the default "
+                        "workload with sequence-major operands)")
     return p.parse_args()
 
 
 COPY_BYTES = 512 * 1024 * 1024
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_N188416_d128.json")
-ROW_TRAFFIC = {r: os.path.join(ROOT, "profiles", f"hbm_traffic_{r}.json") for r in ("merge", "ulysses", "agg")}
+ROW_TRAFFIC = {r: os.path.join(ROOT, "profiles", f"hbm_traffic_{r}.json")
+               for r in ("merge", "ulysses", "agg", "d72", "d160", "bnhd")}
 
 
 KERNEL_FILES = {
@@ -57,6 +61,9 @@ KERNEL_FILES = {
     "merge": ("vitattn_merge.hip",),
     "ulysses": ("vitattn_ulysses.hip",),
     "agg": ("vitattn_agg.hip",),
+    "d72": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
+    "d160": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
+    "bnhd": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
 }
 
 
@@ -343,10 +350,123 @@ def bench_row(args):
     print(json.dumps(line), flush=True)
 
 
+# Attention workloads beside the headline one: the paper's other head dims
+# (Table I's ViT-10B, d = 72 with 64 heads; the 2560-wide 16-head model of
+# Sec. V-C, d = 160) as one GPU's Ulysses shard, and the headline workload
+# with every operand in the sequence-major layout an all-to-all produces.
+ATT_ROWS = {
+    "d72": dict(B=1, H=2, N=65536, d=72, bnhd=False,
+                doc="ViT-10B heads (d=72; 64 heads, 2 per GPU at 32 Ulysses ranks), B=1, N=65,536"),
+    "d160": dict(B=1, H=1, N=65536, d=160, bnhd=False,
+                 doc="2560-wide 16-head model (d=160; 1 head per GPU at 16 Ulysses ranks), B=1, N=65,536"),
+    "bnhd": dict(B=1, H=2, N=188416, d=128, bnhd=True,
+                 doc="B=1, H=2, N=188,416, d=128 with q, k, v, dO, O, dQ, dK, dV all sequence-major [B,N,H,d]"),
+}
+
+
+def bench_attention_row(args):
+    """Forward + backward attention on one of ATT_ROWS: counted TFLOP/s (the
+    headline convention, at the real head dim), the dominant kernel against
+    the bf16 MFMA peak, and the oracle beside it."""
+    import types
+
+    import numpy as np
+    import torch
+
+    import paper_2405_15780_amd as va
+    import workloads
+
+    cfg = ATT_ROWS[args.row]
+    B, H, N, d = cfg["B"], cfg["H"], cfg["N"], cfg["d"]
+    scale = 1.0 / np.sqrt(d)
+    x = workloads.make_small_inputs(B, H, N, d, seed=4000 + d)
+    dev = torch.device("cuda:0")
+    f32 = dict(dtype=torch.float32, device=dev)
+
+    def put(bits):
+        t = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16)
+        if cfg["bnhd"]:  # stored [B, N, H, d], handed over as its [B, H, N, d] view
+            return t.transpose(1, 2).contiguous().to(dev).transpose(1, 2)
+        return t.to(dev)
+
+    def out4():
+        if cfg["bnhd"]:
+            return torch.empty((B, N, H, d), **f32).transpose(1, 2)
+        return torch.empty((B, H, N, d), **f32)
+
+    t = {n: put(a) for n, a in x.items()}
+    o, dq, dk, dv = out4(), out4(), out4(), out4()
+    lse = torch.empty((B, H, N), **f32)
+    ws = torch.empty(va.workspace_bytes(B, H, N, d) // 4, **f32)
+    nn = float(B * H) * N * N * d
+    if cfg["bnhd"]:  # the strided backward is one entry point (three kernels)
+        segs = [("fwd", lambda: va.fwd(t["q"], t["k"], t["v"], scale, out=(o, lse)), "mfma", 4.0 * nn),
+                ("bwd", lambda: va.bwd(t["q"], t["k"], t["v"], o, lse, t["dout"], scale, workspace=ws,
+                                       out=(dq, dk, dv)), "mfma", 14.0 * nn)]
+    else:
+        segs = [("fwd", lambda: va.fwd(t["q"], t["k"], t["v"], scale, out=(o, lse)), "mfma", 4.0 * nn),
+                ("rowdot", lambda: va.bwd_rowdot(o, t["dout"], lse, ws), "hbm", float(B * H * N) * (6 * d + 12)),
+                ("dkdv", lambda: va.bwd_dkdv(t["q"], t["k"], t["v"], t["dout"], lse, dk, dv, ws, scale), "mfma",
+                 8.0 * nn),
+                ("dq", lambda: va.bwd_dq(t["q"], t["k"], t["v"], t["dout"], lse, dq, ws, scale), "mfma", 6.0 * nn)]
+    for _ in range(args.warmup):
+        for _, fn, _, _ in segs:
+            fn()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(segs) + 1)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(args.steps):
+        for j, (_, fn, _, _) in enumerate(segs):
+            ev[i][j].record()
+            fn()
+        ev[i][-1].record()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    seg_ms = {name: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev])) for j, (name, *_) in enumerate(segs)}
+    value = 14.0 * nn / (ms * 1e-3) / 1e12
+    dom = max(seg_ms, key=seg_ms.get)
+    _, _, bound, work = next(s_ for s_ in segs if s_[0] == dom)
+    achieved = work / (seg_ms[dom] * 1e-3) / 1e12
+    per_kernel = {}
+    for name, _, b_, wk in segs:
+        per_kernel[name] = {"ms": seg_ms[name]}
+        if b_ == "mfma":
+            per_kernel[name]["tflops"] = wk / (seg_ms[name] * 1e-3) / 1e12
+        else:
+            per_kernel[name]["gbs"] = wk / (seg_ms[name] * 1e-3) / 1e9
+    line = {
+        "metric": f"attention fwd+bwd TFLOP/s, {cfg['doc']}", "value": value, "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": cfg["doc"], "B": B, "H": H, "N": N, "d": d,
+                   "layout": "[B,N,H,d]" if cfg["bnhd"] else "[B,H,N,d]",
+                   "tile_width": 64 if d <= 64 else 96 if d <= 96 else 128 if d <= 128 else 160},
+        "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
+        "kernels": per_kernel,
+        "roofline": {"bound": bound, "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": stored_traffic(dom, args.row, args.row),
+                     "kernel": dom if dom != "bwd" else "bwd (rowdot + dkdv + dq)",
+                     "algorithmic_flops": work},
+        "kernel_sources": kernel_sources_digest(args.row),
+    }
+    if not args.no_cpu_baseline:
+        w = types.SimpleNamespace(N=N, d=d, scale=scale, backward=True, B=B, H=H)
+        line["cpu_baseline"] = cpu_baseline(w, x, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.row in ATT_ROWS:
+        if args.gpus != 1:
+            print(json.dumps({"error": "this build runs on one GPU only", "n_gpus": args.gpus}))
+            sys.exit(2)
+        bench_attention_row(args)
         return
     if args.row != "attention":
         if args.gpus != 1:

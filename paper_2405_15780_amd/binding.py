@@ -226,13 +226,20 @@ def merge(o_parts, lse_parts, out=None):
     return o, lse
 
 
+def _require_dense(*ts):
+    if not _dense(*ts):
+        raise TypeError("the backward stage entry points take dense [B, H, N, d] tensors; use bwd() for strided ones")
+
+
 def bwd_rowdot(o, dout, lse, workspace):
+    _require_dense(o, dout, lse)
     B, H, N, d = dout.shape
     _check(library().vitattn_bwd_rowdot(o.data_ptr(), dout.data_ptr(), lse.data_ptr(), B, H, N, d, workspace.data_ptr(),
                                         workspace.numel() * workspace.element_size(), _stream_ptr(dout)))
 
 
 def bwd_dkdv(q, k, v, dout, lse, dk, dv, workspace, scale=None):
+    _require_dense(q, k, v, dout, lse, dk, dv)
     B, H, N, d = q.shape
     _check(library().vitattn_bwd_dkdv(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
                                       dk.data_ptr(), dv.data_ptr(), B, H, N, d, _default_scale(d, scale),
@@ -241,6 +248,7 @@ def bwd_dkdv(q, k, v, dout, lse, dk, dv, workspace, scale=None):
 
 
 def bwd_dq(q, k, v, dout, lse, dq, workspace, scale=None):
+    _require_dense(q, k, v, dout, lse, dq)
     B, H, N, d = q.shape
     _check(library().vitattn_bwd_dq(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
                                     dq.data_ptr(), B, H, N, d, _default_scale(d, scale), workspace.data_ptr(),

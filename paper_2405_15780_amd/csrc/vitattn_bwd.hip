@@ -179,7 +179,9 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // One tile of one role, in ring slot SL. Role P: S/P/dV; role dS: dP/dS/dK.
   // The row statistics (and role dS's P) of both query blocks are read
   // before `prefetch` requests the next tile, so that none of these LDS
-  // reads has to wait for that DMA.
+  // reads has to wait for that DMA. The widest tile has no registers to
+  // spare for both blocks: there block 1's are read into block 0's
+  // registers once block 0's vector work is done (end of phase 2).
   auto run_tile = [&](auto role_tag, auto slot_tag, int tile, auto&& prefetch) {
     constexpr bool RP = decltype(role_tag)::value;
     constexpr int SL = decltype(slot_tag)::value;
@@ -190,8 +192,10 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 
     f32x16 m1[2];          // S (P) or dP (dS), per query block
     bf16x8 ob[2][2];       // bf16 operands of P or dS [block][contraction step]
-    float4 stat[2][4];     // LSE2 (role P) or D (role dS) of the block's rows
-    uint4 pin4[2][2];      // role dS: the partner's P, as bf16 pairs
+    constexpr bool LEAN = D == 160;
+    constexpr int NSB = LEAN ? 1 : 2;  // query blocks whose side data is held at once
+    float4 stat[NSB][4];   // LSE2 (role P) or D (role dS) of the block's rows
+    uint4 pin4[NSB][2];    // role dS: the partner's P, as bf16 pairs
 
     // A operand of op i
     auto read_a = [&](int i) -> bf16x8 {
@@ -200,12 +204,13 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       return tf.load(RP ? gs : qs, qb * 32 + 16 * (j / NCB), j % NCB);
     };
     auto read_side = [&](int qb) {
+      const int sb = LEAN ? 0 : qb;
 #pragma unroll
       for (int g = 0; g < 4; ++g)
-        stat[qb][g] = *reinterpret_cast<const float4*>(st + (RP ? kDkvBQ : 0) + qb * 32 + 8 * g + 4 * h);
+        stat[sb][g] = *reinterpret_cast<const float4*>(st + (RP ? kDkvBQ : 0) + qb * 32 + 8 * g + 4 * h);
       if constexpr (!RP) {
-        pin4[qb][0] = xb[qb][0][lane];
-        pin4[qb][1] = xb[qb][1][lane];
+        pin4[sb][0] = xb[qb][0][lane];
+        pin4[sb][1] = xb[qb][1][lane];
       }
     };
     auto valu = [&](int qb, int u) {
@@ -215,12 +220,13 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       for (int rr = 0; rr < RMAX; ++rr) {
         const int r = (u * 16 + PH - 1) / PH + rr;
         if (r >= ((u + 1) * 16 + PH - 1) / PH) break;
-        const float sv = stat[qb][r >> 2][r & 3];
+        const int sb = LEAN ? 0 : qb;
+        const float sv = stat[sb][r >> 2][r & 3];
         float x;
         if constexpr (RP) {
           x = __builtin_amdgcn_exp2f(__builtin_fmaf(m1[qb][r], c, -sv));
         } else {
-          const unsigned w = pin4[qb][r >> 3][(r & 7) >> 1];
+          const unsigned w = pin4[sb][r >> 3][(r & 7) >> 1];
           const float p = __uint_as_float((r & 1) ? (w & 0xffff0000u) : (w << 16));
           x = p * (m1[qb][r] - sv);
         }
@@ -231,27 +237,31 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     };
 
     read_side(0);
-    read_side(1);
+    if constexpr (!LEAN) read_side(1);
     bf16x8 aq[3];
     aq[0] = read_a(0);
     aq[1] = read_a(1);
     sched_fence();
     prefetch();
     sched_fence();
-#pragma unroll
-    for (int i = 0; i < NOPS; ++i) {
-      if (i + 2 < NOPS) aq[(i + 2) % 3] = read_a(i + 2);
-      const int ph = i / PH, j = i % PH, qb = ph & 1;
-      if (ph < 2) {
-        if (j == 0) m1[qb] = zero16();
+    // every op index a compile-time constant (the widest tile's stream is too
+    // long for the unroller's size limit, and register arrays indexed at run
+    // time would live in scratch memory)
+    static_for<0, NOPS>([&](auto IC) __attribute__((always_inline)) {
+      constexpr int i = decltype(IC)::value;
+      constexpr int ph = i / PH, j = i % PH, qb = ph & 1;
+      if constexpr (i + 2 < NOPS) aq[(i + 2) % 3] = read_a(i + 2);
+      if constexpr (ph < 2) {
+        if constexpr (j == 0) m1[qb] = zero16();
         m1[qb] = mfma32(aq[i % 3], hf[j], m1[qb]);
-        if (ph == 1) valu(0, j);
+        if constexpr (ph == 1) valu(0, j);
+        if constexpr (LEAN && i == 2 * PH - 1) read_side(1);
       } else {
         acc[j % NCB] = mfma32(aq[i % 3], ob[qb][j / NCB], acc[j % NCB]);
-        if (ph == 2) valu(1, j);
+        if constexpr (ph == 2) valu(1, j);
       }
       sched_fence();
-    }
+    });
     if constexpr (RP) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
