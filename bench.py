@@ -42,6 +42,11 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 512 MiB device copy (to scale rocprofv3 FETCH_SIZE/WRITE_SIZE)")
+    p.add_argument("--bwd-mode", choices=["auto", "recompute", "stored-ds"], default="auto",
+                   help="backward pass of the default workload: recompute S and dP for dQ, or dQ from the dS "
+                        "blocks the dK/dV kernel stores (a B*H*N^2*2-byte workspace); auto = stored-ds when it fits")
+    p.add_argument("--no-compare", action="store_true",
+                   help="skip timing the other backward mode after the timed region (for profiler runs)")
     p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg", "d72", "d160", "bnhd"],
                    default="attention",
                    help="which workload to time (default: the attention forward+backward hot path at "
@@ -495,10 +500,19 @@ def main():
     o = torch.empty((B, H, N, d), **f32)
     lse = torch.empty((B, H, N), **f32)
     dq, dk, dv = (torch.empty((B, H, N, d), **f32) for _ in range(3))
-    ws = torch.empty(va.workspace_bytes(B, H, N, d) // 4, **f32)
     scale = w.scale
+    # backward mode: the dS mode needs B*H*N^2*2 bytes of workspace (142 GB here)
+    ds_bytes = va.workspace_bytes_kv(B, H, N, N, d, va.VITATTN_BWD_STORE_DS)
+    free_bytes = torch.cuda.mem_get_info(dev)[0]
+    fits = ds_bytes > 0 and ds_bytes + (8 << 30) < free_bytes
+    mode = args.bwd_mode if args.bwd_mode != "auto" else ("stored-ds" if fits and w.backward else "recompute")
+    if mode == "stored-ds" and not fits:
+        print(json.dumps({"error": f"the dS-mode workspace ({ds_bytes / 1e9:.0f} GB) does not fit"}))
+        sys.exit(2)
+    ws = torch.empty(max(ds_bytes if mode == "stored-ds" else va.workspace_bytes(B, H, N, d), 4) // 4, **f32)
 
-    def step(ev=None):
+    def step(ev=None, m=None):
+        m = m or mode
         if ev is not None:
             ev[0].record()
         va.fwd(t["q"], t["k"], t["v"], scale, out=(o, lse))
@@ -508,10 +522,16 @@ def main():
             va.bwd_rowdot(o, t["dout"], lse, ws)
             if ev is not None:
                 ev[2].record()
-            va.bwd_dkdv(t["q"], t["k"], t["v"], t["dout"], lse, dk, dv, ws, scale)
+            if m == "stored-ds":
+                va.bwd_dkdv_ds(t["q"], t["k"], t["v"], t["dout"], lse, dk, dv, ws, scale)
+            else:
+                va.bwd_dkdv(t["q"], t["k"], t["v"], t["dout"], lse, dk, dv, ws, scale)
             if ev is not None:
                 ev[3].record()
-            va.bwd_dq(t["q"], t["k"], t["v"], t["dout"], lse, dq, ws, scale)
+            if m == "stored-ds":
+                va.bwd_dq_from_ds(t["k"], dq, ws, scale)
+            else:
+                va.bwd_dq(t["q"], t["k"], t["v"], t["dout"], lse, dq, ws, scale)
         if ev is not None:
             ev[4].record()
 
@@ -548,16 +568,20 @@ def main():
         "dq": ("mfma", 6.0 * nn),                        # S, dP recomputed; dQ += dS K
         "rowdot": ("hbm", float(B * H * N) * (2 * d + 4 * d + 12)),  # read dO bf16, O fp32, LSE; write D, LSE2
     }
+    if mode == "stored-ds":  # dK/dV also writes dS; dQ = dS K reads it (bound by HBM: 2 bytes per score)
+        kern_work["dkdv"] = ("mfma", 8.0 * nn)
+        kern_work["dq"] = ("hbm", float(B * H) * N * N * 2 + float(B * H * N) * d * 4)
     dom = max(names, key=lambda n: kern_ms[n])
     bound, work = kern_work[dom]
+    traffic_key = w.name if mode == "recompute" else w.name + "+stored-ds"
     if bound == "mfma":
         achieved = work / (kern_ms[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": stored_traffic(dom, w.name), "kernel": dom}
+                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": stored_traffic(dom, traffic_key), "kernel": dom}
     else:
         achieved = work / (kern_ms[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": achieved / PEAK_HBM_GBS, "traffic": stored_traffic(dom, w.name), "kernel": dom}
+                "frac": achieved / PEAK_HBM_GBS, "traffic": stored_traffic(dom, traffic_key), "kernel": dom}
 
     per_kernel = {}
     for n in names:
@@ -568,6 +592,23 @@ def main():
             per_kernel[n]["frac_of_peak"] = per_kernel[n]["tflops"] / PEAK_BF16_TFLOPS
         else:
             per_kernel[n]["gbs"] = wk / (kern_ms[n] * 1e-3) / 1e9
+
+    # the other backward mode, outside the timed region, for comparison
+    alt = None
+    if w.backward and fits and not args.no_compare:
+        other = "recompute" if mode == "stored-ds" else "stored-ds"
+        if other == "stored-ds" and ws.numel() * 4 < ds_bytes:
+            ws = torch.empty(ds_bytes // 4, **f32)
+        for _ in range(max(1, args.warmup)):
+            step(m=other)
+        ev2 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            step(ev2[i], m=other)
+        torch.cuda.synchronize()
+        alt_ms = float(np.mean([e[0].elapsed_time(e[4]) for e in ev2]))
+        alt = {"bwd_mode": other, "ms_per_step": alt_ms, "value": flops["total"] / (alt_ms * 1e-3) / 1e12,
+               "kernels_ms": {n: float(np.mean([e[spans[n][0]].elapsed_time(e[spans[n][1]]) for e in ev2]))
+                              for n in names}}
 
     smi_summary = smi.summary()
     clock = None
@@ -589,7 +630,9 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "B": B, "H": H, "N": N, "d": d, "passes": "fwd+bwd" if w.backward else "fwd",
-                   "grid": f"{w.grid[0]}x{w.grid[1]}", "seed": w.seed},
+                   "grid": f"{w.grid[0]}x{w.grid[1]}", "seed": w.seed, "bwd_mode": mode,
+                   "workspace_gb": ws.numel() * 4 / 1e9},
+        "other_bwd_mode": alt,
         "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "counted_tflop_per_step": flops["total"] / 1e12,
         "step_ms_median": float(np.median(step_ms)),

@@ -140,8 +140,27 @@ int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout
 int vitattn_fwd_kv(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int Nq, int Nk,
                    int d, float scale, void* stream);
 
-/* flags of vitattn_bwd_kv */
+/* flags of vitattn_bwd_kv and vitattn_bwd_strided */
 #define VITATTN_BWD_ACCUMULATE_DQ 1 /* dq += this segment's share instead of dq = it */
+#define VITATTN_BWD_STORE_DS 2      /* dS mode: dQ from stored dS (see vitattn_bwd_workspace_bytes_kv) */
+
+/*
+ * Workspace bytes of vitattn_bwd_kv / vitattn_bwd_strided for these sizes
+ * and flags; 0 for invalid arguments. Without VITATTN_BWD_STORE_DS it equals
+ * vitattn_bwd_workspace_bytes(B, H, Nq, d).
+ *
+ * The dS mode trades memory for matrix-core work. The dK/dV kernel already
+ * forms dS = P o (dP - D) (bf16, the value it multiplies into dK); with
+ * VITATTN_BWD_STORE_DS it also writes every dS block to the workspace, and dQ
+ * = scale dS K then streams them (2 d flops per score) instead of recomputing
+ * S and dP in a third kernel (6 d flops per score). The extra workspace is
+ * 2 bytes per (query, key) pair of every head, rounded up to 64 queries and
+ * 128 keys: B*H*Nq*Nk*2 bytes, 142 GB at B=1, H=2, N=188,416. Results differ
+ * from the default mode only in the rounding of dS (the default dQ kernel
+ * rounds an fp32 P times (dP - D) to bf16, this one a bf16 P times it).
+ * Requires Nq <= 16,777,152.
+ */
+size_t vitattn_bwd_workspace_bytes_kv(int B, int H, int Nq, int Nk, int d, int flags);
 
 /*
  * Backward pass of Nq queries over Nk keys (vitattn_bwd is the case
@@ -155,8 +174,11 @@ int vitattn_fwd_kv(const void* q, const void* k, const void* v, float* o, float*
  *   flags    : 0, or VITATTN_BWD_ACCUMULATE_DQ to add the share to dq (sum
  *              the segments of one key set by calling once per segment on
  *              one stream with dq zeroed first; the order of the sum is the
- *              order of the calls). Other bits: VITATTN_E_INVAL.
- *   workspace: at least vitattn_bwd_workspace_bytes(B, H, Nq, d) bytes.
+ *              order of the calls), and/or VITATTN_BWD_STORE_DS (below).
+ *              Other bits: VITATTN_E_INVAL.
+ *   workspace: at least vitattn_bwd_workspace_bytes_kv(B, H, Nq, Nk, d, flags)
+ *              bytes (vitattn_bwd_workspace_bytes(B, H, Nq, d) without
+ *              VITATTN_BWD_STORE_DS), else VITATTN_E_WORKSPACE.
  */
 int vitattn_bwd_kv(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
                    float* dq, float* dk, float* dv, int B, int H, int Nq, int Nk, int d, float scale, int flags,
@@ -195,6 +217,17 @@ int vitattn_bwd_strided(const void* q, vitattn_strides sq, const void* k, vitatt
                         vitattn_strides sdo, const float* lse, float* dq, vitattn_strides sdq, float* dk,
                         vitattn_strides sdk, float* dv, vitattn_strides sdv, int B, int H, int Nq, int Nk, int d,
                         float scale, int flags, void* workspace, size_t workspace_bytes, void* stream);
+
+/* The two kernels of the dS mode as separate calls (dense operands, Nq = Nk =
+ * N; the row-statistics stage vitattn_bwd_rowdot runs first), for timing each:
+ * vitattn_bwd_dkdv_ds writes dK, dV and the dS blocks into the workspace,
+ * vitattn_bwd_dq_from_ds then writes dQ from them. The workspace must hold
+ * vitattn_bwd_workspace_bytes_kv(B, H, N, N, d, VITATTN_BWD_STORE_DS) bytes. */
+int vitattn_bwd_dkdv_ds(const void* q, const void* k, const void* v, const void* dout, const float* lse, float* dk,
+                        float* dv, int B, int H, int N, int d, float scale, void* workspace, size_t workspace_bytes,
+                        void* stream);
+int vitattn_bwd_dq_from_ds(const void* k, float* dq, int B, int H, int N, int d, float scale, const void* workspace,
+                           size_t workspace_bytes, void* stream);
 
 /* largest number of partial results vitattn_merge accepts */
 #define VITATTN_MERGE_MAX_PARTS 65536

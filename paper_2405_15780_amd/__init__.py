@@ -9,13 +9,16 @@ fallback path.
 from .binding import (  # noqa: F401
     LIB_PATH,
     VITATTN_BWD_ACCUMULATE_DQ,
+    VITATTN_BWD_STORE_DS,
     Strides,
     VitattnError,
     agg_bwd,
     agg_fwd,
     bwd,
     bwd_dkdv,
+    bwd_dkdv_ds,
     bwd_dq,
+    bwd_dq_from_ds,
     bwd_rowdot,
     fwd,
     library,
@@ -28,4 +31,5 @@ from .binding import (  # noqa: F401
     ulysses_unpack_out,
     version,
     workspace_bytes,
+    workspace_bytes_kv,
 )

@@ -36,6 +36,9 @@ _SIGNATURES = {
     "vitattn_bwd_dq": (c_int, [c_void_p] * 6 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
     "vitattn_fwd_kv": (c_int, [c_void_p] * 5 + [c_int] * 5 + [c_float, c_void_p]),
     "vitattn_bwd_kv": (c_int, [c_void_p] * 9 + [c_int] * 5 + [c_float, c_int, c_void_p, c_size_t, c_void_p]),
+    "vitattn_bwd_workspace_bytes_kv": (c_size_t, [c_int] * 6),
+    "vitattn_bwd_dkdv_ds": (c_int, [c_void_p] * 7 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
+    "vitattn_bwd_dq_from_ds": (c_int, [c_void_p] * 2 + [c_int] * 4 + [c_float, c_void_p, c_size_t, c_void_p]),
     "vitattn_fwd_strided": (c_int, [c_void_p, _S] * 4 + [c_void_p] + [c_int] * 5 + [c_float, c_void_p]),
     "vitattn_bwd_strided": (c_int, [c_void_p, _S] * 5 + [c_void_p] + [c_void_p, _S] * 3 + [c_int] * 5
                             + [c_float, c_int, c_void_p, c_size_t, c_void_p]),
@@ -124,6 +127,12 @@ def _default_scale(d, scale):
 
 
 VITATTN_BWD_ACCUMULATE_DQ = 1
+VITATTN_BWD_STORE_DS = 2
+
+
+def workspace_bytes_kv(B: int, H: int, Nq: int, Nk: int, d: int, flags: int = 0) -> int:
+    """Workspace bytes of the backward pass for these sizes and flags (0 if invalid)."""
+    return int(library().vitattn_bwd_workspace_bytes_kv(B, H, Nq, Nk, d, flags))
 
 
 def _kv_shapes(q, k, v):
@@ -160,24 +169,27 @@ def fwd(q, k, v, scale=None, out=None):
     return o, lse
 
 
-def _workspace(q, workspace):
+def _workspace(q, k, workspace, flags=0):
     torch = _torch()
     B, H, N, d = q.shape
-    need = workspace_bytes(B, H, N, d)
+    need = workspace_bytes_kv(B, H, N, k.shape[2], d, flags)
     if workspace is None:
-        workspace = torch.empty(need // 4, dtype=torch.float32, device=q.device)
+        workspace = torch.empty(max(need, 4) // 4, dtype=torch.float32, device=q.device)
     return workspace, workspace.numel() * workspace.element_size()
 
 
-def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None, accumulate_dq=False):
+def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None, accumulate_dq=False, store_ds=False):
     """dQ (fp32 [B,H,Nq,d]), dK, dV (fp32 [B,H,Nk,d]) for the upstream gradient
     dout (bf16). For one key segment pass the merged o and lse of all keys;
-    accumulate_dq adds this segment's share to out[0] instead of overwriting."""
+    accumulate_dq adds this segment's share to out[0] instead of overwriting.
+    store_ds selects the dS mode (dQ from stored dS; a workspace of about
+    B*H*Nq*Nk*2 bytes, see workspace_bytes_kv)."""
     torch = _torch()
     for t, n in ((q, "q"), (k, "k"), (v, "v"), (dout, "dout")):
         _as_input(t, n)
     B, H, Nq, Nk, d = _kv_shapes(q, k, v)
-    ws, ws_bytes = _workspace(q, workspace)
+    flags = (VITATTN_BWD_ACCUMULATE_DQ if accumulate_dq else 0) | (VITATTN_BWD_STORE_DS if store_ds else 0)
+    ws, ws_bytes = _workspace(q, k, workspace, flags)
     if out is None:
         if accumulate_dq:
             raise ValueError("accumulate_dq needs out=(dq, dk, dv) holding the running dq")
@@ -191,17 +203,15 @@ def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None, accumulate_
                                      strides_of(v), o.data_ptr(), strides_of(o), dout.data_ptr(), strides_of(dout),
                                      lse.data_ptr(), dq.data_ptr(), strides_of(dq), dk.data_ptr(), strides_of(dk),
                                      dv.data_ptr(), strides_of(dv), B, H, Nq, Nk, d, _default_scale(d, scale),
-                                     VITATTN_BWD_ACCUMULATE_DQ if accumulate_dq else 0, ws.data_ptr(), ws_bytes,
-                                     _stream_ptr(q))
-    elif Nq == Nk and not accumulate_dq:
+                                     flags, ws.data_ptr(), ws_bytes, _stream_ptr(q))
+    elif Nq == Nk and flags == 0:
         st = lib.vitattn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(), lse.data_ptr(),
                              dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, Nq, d, _default_scale(d, scale),
                              ws.data_ptr(), ws_bytes, _stream_ptr(q))
     else:
         st = lib.vitattn_bwd_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(),
                                 lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, Nq, Nk, d,
-                                _default_scale(d, scale), VITATTN_BWD_ACCUMULATE_DQ if accumulate_dq else 0,
-                                ws.data_ptr(), ws_bytes, _stream_ptr(q))
+                                _default_scale(d, scale), flags, ws.data_ptr(), ws_bytes, _stream_ptr(q))
     _check(st)
     return dq, dk, dv
 
@@ -245,6 +255,25 @@ def bwd_dkdv(q, k, v, dout, lse, dk, dv, workspace, scale=None):
                                       dk.data_ptr(), dv.data_ptr(), B, H, N, d, _default_scale(d, scale),
                                       workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                       _stream_ptr(q)))
+
+
+def bwd_dkdv_ds(q, k, v, dout, lse, dk, dv, workspace, scale=None):
+    """The dK/dV stage of the dS mode (also writes the dS blocks into workspace)."""
+    _require_dense(q, k, v, dout, lse, dk, dv)
+    B, H, N, d = q.shape
+    _check(library().vitattn_bwd_dkdv_ds(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
+                                         dk.data_ptr(), dv.data_ptr(), B, H, N, d, _default_scale(d, scale),
+                                         workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                         _stream_ptr(q)))
+
+
+def bwd_dq_from_ds(k, dq, workspace, scale=None):
+    """The dQ stage of the dS mode, from the dS blocks bwd_dkdv_ds stored."""
+    _require_dense(k, dq)
+    B, H, N, d = k.shape
+    _check(library().vitattn_bwd_dq_from_ds(k.data_ptr(), dq.data_ptr(), B, H, N, d, _default_scale(d, scale),
+                                            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                            _stream_ptr(k)))
 
 
 def bwd_dq(q, k, v, dout, lse, dq, workspace, scale=None):

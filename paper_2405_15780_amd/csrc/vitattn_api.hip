@@ -117,6 +117,20 @@ size_t vitattn_bwd_workspace_bytes(int B, int H, int N, int d) {
   return 2 * vitattn::bwd_region_floats((long long)B * H * N) * sizeof(float);
 }
 
+// the dS region's 32-query block rows must stay within 31-bit buffer offsets
+static bool ds_mode_ok(int Nq) { return (long long)vitattn::ds_query_blocks(Nq) * 2048 <= 0x7fffffffLL; }
+
+size_t vitattn_bwd_workspace_bytes_kv(int B, int H, int Nq, int Nk, int d, int flags) {
+  if (check_sizes_kv(B, H, Nq, Nk, d) != VITATTN_OK) return 0;
+  if ((flags & ~(VITATTN_BWD_ACCUMULATE_DQ | VITATTN_BWD_STORE_DS)) != 0) return 0;
+  size_t bytes = vitattn_bwd_workspace_bytes(B, H, Nq, d);
+  if (flags & VITATTN_BWD_STORE_DS) {
+    if (!ds_mode_ok(Nq)) return 0;
+    bytes += vitattn::ds_region_bytes((long long)B * H, Nq, Nk);
+  }
+  return bytes;
+}
+
 int vitattn_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int B, int H, int N, int d,
                 float scale, void* stream) {
   return vitattn_fwd_kv(q, k, v, o, lse, B, H, N, N, d, scale, stream);
@@ -186,6 +200,7 @@ static vitattn::BwdArgs bwd_args(const void* q, const void* k, const void* v, co
   a.dv = dv;
   a.drow = static_cast<float*>(const_cast<void*>(workspace));
   a.lse2 = a.drow + vitattn::bwd_region_floats((long long)B * H * Nq);
+  a.ds = nullptr;
   a.mq = a.mo = a.mg = a.mdq = to_map(dense(H, Nq, d));
   a.mk = a.mv = a.mdk = a.mdv = to_map(dense(H, Nk, d));
   a.H = H;
@@ -226,16 +241,20 @@ int vitattn_bwd_strided(const void* q, vitattn_strides sq, const void* k, vitatt
         !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
       return VITATTN_E_INVAL;
     if (!scale_ok(scale)) return VITATTN_E_INVAL;
-    if ((flags & ~VITATTN_BWD_ACCUMULATE_DQ) != 0) return VITATTN_E_INVAL;
+    if ((flags & ~(VITATTN_BWD_ACCUMULATE_DQ | VITATTN_BWD_STORE_DS)) != 0) return VITATTN_E_INVAL;
+    if ((flags & VITATTN_BWD_STORE_DS) && !ds_mode_ok(Nq)) return VITATTN_E_INVAL;
     if (check_map(sq, B, H, Nq, d, 2, false) || check_map(sk, B, H, Nk, d, 2, false) ||
         check_map(sv, B, H, Nk, d, 2, false) || check_map(so, B, H, Nq, d, 4, false) ||
         check_map(sdo, B, H, Nq, d, 2, false) || check_map(sdq, B, H, Nq, d, 4, true) ||
         check_map(sdk, B, H, Nk, d, 4, true) || check_map(sdv, B, H, Nk, d, 4, true))
       return VITATTN_E_INVAL;
-    st = check_workspace(workspace, workspace_bytes, B, H, Nq, d);
-    if (st != VITATTN_OK) return st;
+    if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 15u) != 0 ||
+        workspace_bytes < vitattn_bwd_workspace_bytes_kv(B, H, Nq, Nk, d, flags))
+      return VITATTN_E_WORKSPACE;
     vitattn::BwdArgs a = bwd_args(q, k, v, o, dout, lse, dq, dk, dv, B, H, Nq, Nk, d, scale,
                                   (flags & VITATTN_BWD_ACCUMULATE_DQ) != 0, workspace, stream);
+    if (flags & VITATTN_BWD_STORE_DS)
+      a.ds = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + vitattn_bwd_workspace_bytes(B, H, Nq, d));
     a.mq = to_map(sq);
     a.mk = to_map(sk);
     a.mv = to_map(sv);
@@ -439,6 +458,50 @@ int vitattn_agg_bwd(const void* q, const void* k, const void* v, const float* o,
     a.scale = scale;
     a.stream = static_cast<hipStream_t>(stream);
     return vitattn::launch_agg_bwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+// Stages of the dS-mode backward (dense operands), for timing each kernel.
+int vitattn_bwd_dkdv_ds(const void* q, const void* k, const void* v, const void* dout, const float* lse, float* dk,
+                        float* dv, int B, int H, int N, int d, float scale, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(lse) || !aligned16(dk) ||
+        !aligned16(dv))
+      return VITATTN_E_INVAL;
+    if (!scale_ok(scale) || !ds_mode_ok(N)) return VITATTN_E_INVAL;
+    if (workspace == nullptr || !aligned16(workspace) ||
+        workspace_bytes < vitattn_bwd_workspace_bytes_kv(B, H, N, N, d, VITATTN_BWD_STORE_DS))
+      return VITATTN_E_WORKSPACE;
+    vitattn::BwdArgs a =
+        bwd_args(q, k, v, nullptr, dout, lse, nullptr, dk, dv, B, H, N, N, d, scale, false, workspace, stream);
+    a.ds = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + vitattn_bwd_workspace_bytes(B, H, N, d));
+    return vitattn::launch_bwd_dkdv(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+int vitattn_bwd_dq_from_ds(const void* k, float* dq, int B, int H, int N, int d, float scale, const void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(k) || !aligned16(dq)) return VITATTN_E_INVAL;
+    if (!scale_ok(scale) || !ds_mode_ok(N)) return VITATTN_E_INVAL;
+    if (workspace == nullptr || !aligned16(workspace) ||
+        workspace_bytes < vitattn_bwd_workspace_bytes_kv(B, H, N, N, d, VITATTN_BWD_STORE_DS))
+      return VITATTN_E_WORKSPACE;
+    vitattn::BwdArgs a =
+        bwd_args(nullptr, k, nullptr, nullptr, nullptr, nullptr, dq, nullptr, nullptr, B, H, N, N, d, scale, false,
+                 workspace, stream);
+    a.ds = reinterpret_cast<uint16_t*>(static_cast<char*>(const_cast<void*>(workspace)) +
+                                       vitattn_bwd_workspace_bytes(B, H, N, d));
+    return vitattn::launch_bwd_dq(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
   } catch (...) {
     return VITATTN_E_INTERNAL;
   }

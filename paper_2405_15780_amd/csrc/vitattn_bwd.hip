@@ -95,12 +95,20 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 //   2. first product of block 1;  vector units: P or dS of block 0
 //   3. second product of block 0 (dV or dK);  vector units: block 1
 //   4. second product of block 1
-template <int D>
+//
+// With STORE_DS the dS waves also write every dS block they form (bf16, the
+// operand of their dK product) to ds_out, for the dQ-from-dS kernel below.
+// A tile's blocks are stored at the start of the wave's next tile, before
+// that tile's DMA requests: loads and stores share one completion counter
+// and may complete out of order with respect to each other, so a store must
+// never sit between a DMA request and the wait for it.
+template <int D, bool STORE_DS>
 __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
-    float* __restrict__ dk, float* __restrict__ dv, const Map mq, const Map mk, const Map mv, const Map mg,
-    const Map mdk, const Map mdv, int H, int dr, int Nq, int Nk, int n_ktiles, int total, float c, float scale) {
+    float* __restrict__ dk, float* __restrict__ dv, uint16_t* __restrict__ ds_out, const Map mq, const Map mk,
+    const Map mv, const Map mg, const Map mdk, const Map mdv, int H, int dr, int Nq, int Nk, int n_ktiles, int total,
+    float c, float scale) {
   constexpr int KK = D / 16, NCB = D / 32;
   constexpr int PH = KK;           // ops per phase
   constexpr int NOPS = 4 * PH;     // ops per tile
@@ -156,9 +164,12 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) hf[kk] = as_bf16x8(buffer_load16(rh, chunk_offset(key, 2 * kk + h, ldh, chr)));
 
-  TileDma<D, kDkvBQ, NWAVES> dma, dmg;  // Q and dO tiles
-  dma.init(wave, lane, ldq, chr);
-  dmg.init(wave, lane, ldg, chr);
+  // Q and dO tiles. With STORE_DS only the four role-P waves fetch tiles, so
+  // the dS waves never wait for a DMA request (and with it, for their stores).
+  constexpr int DMA_WAVES = STORE_DS ? kBwdWaves : NWAVES;
+  TileDma<D, kDkvBQ, DMA_WAVES> dma, dmg;
+  dma.init(wave % DMA_WAVES, lane, ldq, chr);
+  dmg.init(wave % DMA_WAVES, lane, ldg, chr);
   RowFrag<D> rf;
   rf.init(lane);
   TrFrag<D> tf;
@@ -168,6 +179,27 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   f32x16 acc[NCB];  // dV^T (role P) or dK^T (role dS)
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero16();
+
+  // STORE_DS: the dS operands of the wave's previous tile, not yet stored
+  const int n_qt_real = (Nq + kDkvBQ - 1) / kDkvBQ;
+  bf16x8 pend[2][2];
+  int pend_tile = -1;
+  auto flush_ds = [&]() {
+    if constexpr (STORE_DS) {
+      if (pend_tile >= 0 && pend_tile < n_qt_real) {
+        // blocks (key block, query blocks 2t and 2t+1) of this head, 2 KB each
+        const size_t nkb = (size_t)n_ktiles * kBwdWaves, nqb = 2 * (size_t)n_qt_real;
+        uint16_t* dst = ds_out + (((size_t)bh * nkb + (size_t)kt * kBwdWaves + kb) * nqb + 2 * pend_tile) * 1024;
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks)
+            __builtin_nontemporal_store(pend[qb][ks],
+                                        reinterpret_cast<bf16x8*>(dst + qb * 1024 + ks * 512 + lane * 8));
+      }
+      pend_tile = -1;
+    }
+  };
 
   auto issue_tile = [&](auto slot_tag, int t) {
     constexpr int SL = decltype(slot_tag)::value;
@@ -236,6 +268,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       }
     };
 
+    if constexpr (!RP) flush_ds();  // the previous tile's dS, before this tile's DMA requests
     read_side(0);
     if constexpr (!LEAN) read_side(1);
     bf16x8 aq[3];
@@ -267,6 +300,12 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) xb[qb][ks][lane] = __builtin_bit_cast(uint4, ob[qb][ks]);
+    } else if constexpr (STORE_DS) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) pend[qb][ks] = ob[qb][ks];
+      pend_tile = tile;
     }
   };
 
@@ -280,30 +319,78 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // iterations 1 .. n_pad-1 run in groups of three with fixed slots.
   const int n_qt = (Nq + kDkvBQ - 1) / kDkvBQ;
   const int n_pad = n_qt + (3 + 1 - n_qt % 3) % 3;
-  auto iteration = [&](auto slot_p, auto slot_next, auto slot_ds, int t, bool do_p, bool do_ds) {
+  // Each role runs its own copy of the tile loop, so that the compiler sees
+  // in the dS waves' copy that (with STORE_DS) they never have a DMA request
+  // in flight, and adds no wait for one; both copies pass the same barriers.
+  // End of an iteration: the fetched tile is in LDS and every wave is done
+  // with the slot refilled next. With STORE_DS the dS waves issued no loads
+  // and skip the wait (their stores drain in the background); a plain
+  // barrier then keeps the compiler from adding a wait for every access.
+  auto iteration = [&](auto role_tag, auto slot_p, auto slot_next, auto slot_ds, int t, bool run) {
+    constexpr bool RP = decltype(role_tag)::value;
     // tile t+1 past the end: zero rows, never read
-    auto prefetch = [&]() { issue_tile(slot_next, t + 1); };
-    if (role_p) {
-      if (do_p) run_tile(RoleP{}, slot_p, t, prefetch);
+    auto prefetch = [&]() {
+      if constexpr (!STORE_DS || RP) issue_tile(slot_next, t + 1);
+    };
+    if constexpr (RP) {
+      if (run) run_tile(RoleP{}, slot_p, t, prefetch);
       else prefetch();
     } else {
-      if (do_ds) run_tile(RoleDs{}, slot_ds, t - 1, prefetch);
+      if (run) run_tile(RoleDs{}, slot_ds, t - 1, prefetch);
       else prefetch();
     }
-    wait_vmem();
-    __syncthreads();
+    if constexpr (STORE_DS) {
+      if constexpr (RP) wait_vmem();
+      barrier_lds();
+    } else {
+      wait_vmem();
+      __syncthreads();
+    }
   };
-  issue_tile(S0{}, 0);
+  auto run_role = [&](auto role_tag) {
+    constexpr bool RP = decltype(role_tag)::value;
+    iteration(role_tag, S0{}, S1{}, S2{}, 0, RP);
+    for (int t = 1; t < n_pad; t += 3) {
+      iteration(role_tag, S1{}, S2{}, S0{}, t, true);
+      iteration(role_tag, S2{}, S0{}, S1{}, t + 1, true);
+      iteration(role_tag, S0{}, S1{}, S2{}, t + 2, true);
+    }
+    // last: role dS on tile n_pad-1 (slot 0, since n_pad = 1 mod 3)
+    if constexpr (!RP) {
+      run_tile(RoleDs{}, S0{}, n_pad - 1, [] {});
+      flush_ds();
+    }
+  };
+  if (!STORE_DS || role_p) issue_tile(S0{}, 0);
   wait_vmem();
   __syncthreads();
-  iteration(S0{}, S1{}, S2{}, 0, true, false);
-  for (int t = 1; t < n_pad; t += 3) {
-    iteration(S1{}, S2{}, S0{}, t, true, true);
-    iteration(S2{}, S0{}, S1{}, t + 1, true, true);
-    iteration(S0{}, S1{}, S2{}, t + 2, true, true);
+  if constexpr (STORE_DS) {
+    if (role_p)
+      run_role(RoleP{});
+    else
+      run_role(RoleDs{});
+  } else {
+    // one loop for both roles (this form keeps the default kernel's register
+    // allocation; the role is a run-time branch inside each iteration)
+    auto both = [&](auto slot_p, auto slot_next, auto slot_ds, int t, bool do_p, bool do_ds) {
+      if (role_p) {
+        if (do_p) run_tile(RoleP{}, slot_p, t, [&]() { issue_tile(slot_next, t + 1); });
+        else issue_tile(slot_next, t + 1);
+      } else {
+        if (do_ds) run_tile(RoleDs{}, slot_ds, t - 1, [&]() { issue_tile(slot_next, t + 1); });
+        else issue_tile(slot_next, t + 1);
+      }
+      wait_vmem();
+      __syncthreads();
+    };
+    both(S0{}, S1{}, S2{}, 0, true, false);
+    for (int t = 1; t < n_pad; t += 3) {
+      both(S1{}, S2{}, S0{}, t, true, true);
+      both(S2{}, S0{}, S1{}, t + 1, true, true);
+      both(S0{}, S1{}, S2{}, t + 2, true, true);
+    }
+    if (!role_p) run_tile(RoleDs{}, S0{}, n_pad - 1, [] {});
   }
-  // last: role dS on tile n_pad-1 (slot 0, since n_pad = 1 mod 3)
-  if (!role_p) run_tile(RoleDs{}, S0{}, n_pad - 1, [] {});
   (void)DMA_PER_TILE;
 
   if (key < Nk) {
@@ -547,6 +634,161 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   }
 }
 
+// ------------------------------------------------------------------ dQ from stored dS
+//
+// dQ = scale dS K from the dS blocks the dK/dV kernel stored: a streaming
+// product with no recomputation of S and dP (2 d flops per score instead of
+// 6), bound by reading dS from HBM. Block layout, one block per 32 keys x 32
+// queries of one head: [bh][key block][query block][ks][lane][8] bf16 with
+// ks the 16-query half and lane = 32 h + key, slot t of lane (h, key) holding
+// query 16 ks + 8 (t/4) + 4 h + t%4 (the dK/dV kernel's dS operand order).
+//
+// One workgroup = NW waves x 32 queries of one (b, h); key tiles of 32 stream
+// through a ring of six LDS slots: K (the NW waves split its DMA) and the NW
+// dS blocks of the tile (each wave fetches and reads only its own block). The
+// dQ^T product needs dS^T with one query per lane and 8 keys per slot group,
+// the transpose of the stored order; two ds_read_b64_tr_b16 per 16 keys build
+// it (lane j of a 16-lane group supplies the address of the 4 consecutive
+// queries of key 16 ks + 4 h + j/4, so result lane i gets query i's entry of
+// 4 consecutive keys).
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
+    const uint16_t* __restrict__ k, const uint16_t* __restrict__ ds, float* __restrict__ dq, const Map mk,
+    const Map mdq, int H, int dr, int Nq, int Nk, int n_qtiles, int total, int nkb, int nqb, float scale,
+    int accumulate) {
+  constexpr int BN = 32;
+  constexpr int NCB = D / 32;
+  constexpr int KTILE = BN * D * 2;  // bytes of a K tile
+  constexpr int STILE = NW * 2048;   // bytes of the dS blocks of a tile
+  constexpr int RING = 6;
+  __shared__ __attribute__((aligned(1024))) char kbuf0[KTILE];
+  __shared__ __attribute__((aligned(1024))) char kbuf1[KTILE];
+  __shared__ __attribute__((aligned(1024))) char kbuf2[KTILE];
+  __shared__ __attribute__((aligned(1024))) char kbuf3[KTILE];
+  __shared__ __attribute__((aligned(1024))) char kbuf4[KTILE];
+  __shared__ __attribute__((aligned(1024))) char kbuf5[KTILE];
+  __shared__ __attribute__((aligned(1024))) char sbuf0[STILE];
+  __shared__ __attribute__((aligned(1024))) char sbuf1[STILE];
+  __shared__ __attribute__((aligned(1024))) char sbuf2[STILE];
+  __shared__ __attribute__((aligned(1024))) char sbuf3[STILE];
+  __shared__ __attribute__((aligned(1024))) char sbuf4[STILE];
+  __shared__ __attribute__((aligned(1024))) char sbuf5[STILE];
+  char* const kbuf[RING] = {kbuf0, kbuf1, kbuf2, kbuf3, kbuf4, kbuf5};
+  char* const sbuf[RING] = {sbuf0, sbuf1, sbuf2, sbuf3, sbuf4, sbuf5};
+
+  const int work = xcd_remap(blockIdx.x, total);
+  const int bh = work / n_qtiles;
+  const int qt = work - bh * n_qtiles;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
+  const int qblock = qt * NW + wave;  // this wave's 32-query block
+
+  const int chr = dr >> 3;
+  const int ldk = 2 * mk.ld;
+  const rsrc_t rk = make_rsrc(k + mk.head(bh, H), (unsigned)(Nk * ldk));
+  TileDma<D, BN, NW> dma;
+  dma.init(wave, lane, ldk, chr);
+  TrFrag<D> tf;
+  tf.init(lane);
+  // dS^T operand reads: per-lane byte offset within the wave's 2 KB block
+  const int g = lane >> 4, j = lane & 15;
+  const int soff = (g & 1) * 1024 + (j & 1) * 512 + (4 * (g >> 1) + (j >> 2)) * 16 + 8 * ((j >> 1) & 1);
+
+  // this head's dS rows start here; key block kb's row of nqb blocks follows
+  const uint16_t* ds_head = ds + (size_t)bh * nkb * nqb * 1024;
+  auto issue_tile = [&](int slot_k, char* kdst, char* sdst, int t) {
+    (void)slot_k;
+    dma.issue(rk, t * BN, ldk, kdst);
+    // the wave's own dS block of key block t (zeros past the stored blocks)
+    const rsrc_t rs = make_rsrc(ds_head + (size_t)(t < nkb ? t : 0) * nqb * 1024,
+                                t < nkb ? (unsigned)nqb * 2048u : 0u);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(sdst + wave * 2048 + i * 1024), 16,
+                                               qblock * 2048 + i * 1024 + lane * 16, 0, 0, 0);
+  };
+  // vector loads per wave per tile: its K share (none for the waves left
+  // without one when a K tile is fewer instructions than waves) and 2 for dS
+  constexpr int LOADS = decltype(dma)::PER_WAVE + 2;
+  const bool k_share = decltype(dma)::ALL_ACTIVE || dma.active;
+
+  f32x16 dqacc[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) dqacc[cb] = zero16();
+
+  const int n_kt = (Nk + BN - 1) / BN;
+  const int n_iter = (n_kt + RING - 1) / RING * RING;  // extra tiles: zero K, add nothing
+#pragma unroll
+  for (int t = 0; t < RING - 1; ++t) issue_tile(t, kbuf[t], sbuf[t], t);
+
+  // tile jj in slot SL: wait for its loads (the RING - 2 later tiles stay in
+  // flight), barrier, request tile jj + RING - 1 into the slot of tile jj - 1
+  // (every wave finished reading it before this barrier), then the products.
+  auto stage = [&](auto slot_tag, int jj) {
+    constexpr int SL = decltype(slot_tag)::value;
+    constexpr int NX = (SL + RING - 1) % RING;
+    if (k_share)
+      wait_vmem_leave<(RING - 2) * LOADS>();
+    else
+      wait_vmem_leave<(RING - 2) * 2>();
+    barrier_lds();
+    issue_tile(NX, kbuf[NX], sbuf[NX], jj + RING - 1);
+    const char* ks = kbuf[SL];
+    const char* sb = sbuf[SL] + wave * 2048;
+    bf16x8 dsb[2];
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh) {
+      const char* p0 = sb + soff + kh * 256;
+      bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
+      bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0 + 128));
+      dsb[kh][0] = lo[0]; dsb[kh][1] = lo[1]; dsb[kh][2] = lo[2]; dsb[kh][3] = lo[3];
+      dsb[kh][4] = hi[0]; dsb[kh][5] = hi[1]; dsb[kh][6] = hi[2]; dsb[kh][7] = hi[3];
+    }
+    bf16x8 aq[2];
+    aq[0] = tf.load(ks, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 2 * NCB; ++i) {
+      if (i + 1 < 2 * NCB) aq[(i + 1) & 1] = tf.load(ks, 16 * ((i + 1) / NCB), (i + 1) % NCB);
+      dqacc[i % NCB] = mfma32(aq[i & 1], dsb[i / NCB], dqacc[i % NCB]);
+    }
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  using S4 = std::integral_constant<int, 4>;
+  using S5 = std::integral_constant<int, 5>;
+  for (int jj = 0; jj < n_iter; jj += RING) {
+    stage(S0{}, jj);
+    stage(S1{}, jj + 1);
+    stage(S2{}, jj + 2);
+    stage(S3{}, jj + 3);
+    stage(S4{}, jj + 4);
+    stage(S5{}, jj + 5);
+  }
+  wait_vmem();  // requests past the last tile must land before this LDS is reassigned
+
+  const int qrow = qblock * 32 + (lane & 31);
+  if (qrow < Nq) {
+    float* row = dq + mdq.head(bh, H) + (size_t)qrow * mdq.ld;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        const int col = 32 * cb + 8 * gg + 4 * h;  // d is a multiple of 8: four columns are all in or all out
+        if (col >= dr) continue;
+        float4* dst = reinterpret_cast<float4*>(row + col);
+        float4 val = make_float4(dqacc[cb][4 * gg] * scale, dqacc[cb][4 * gg + 1] * scale,
+                                 dqacc[cb][4 * gg + 2] * scale, dqacc[cb][4 * gg + 3] * scale);
+        if (accumulate) {
+          const float4 prev = *dst;
+          val = make_float4(prev.x + val.x, prev.y + val.y, prev.z + val.z, prev.w + val.w);
+        }
+        *dst = val;
+      }
+  }
+}
+
 // ------------------------------------------------------------------ launch
 
 template <int LPR>
@@ -558,27 +800,56 @@ static hipError_t rowdot_l(const BwdArgs& a) {
   return hipGetLastError();
 }
 
-template <int D>
-static hipError_t dkdv_d(const BwdArgs& a) {
+template <int D, bool STORE_DS>
+static hipError_t dkdv_s(const BwdArgs& a) {
   const int n_kt = (a.Nk + kDkvBK - 1) / kDkvBK;
   const int total = a.BH * n_kt;
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>), dim3(total), dim3(2 * kBwdThreads), 0, a.stream, a.q, a.k, a.v,
-                     a.dout, a.drow, a.lse2, a.dk, a.dv, a.mq, a.mk, a.mv, a.mg, a.mdk, a.mdv, a.H, a.d, a.Nq, a.Nk,
-                     n_kt, total, a.scale * kLog2e, a.scale);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS>), dim3(total), dim3(2 * kBwdThreads), 0, a.stream, a.q,
+                     a.k, a.v, a.dout, a.drow, a.lse2, a.dk, a.dv, a.ds, a.mq, a.mk, a.mv, a.mg, a.mdk, a.mdv, a.H,
+                     a.d, a.Nq, a.Nk, n_kt, total, a.scale * kLog2e, a.scale);
+  return hipGetLastError();
+}
+template <int D>
+static hipError_t dkdv_d(const BwdArgs& a) {
+  return a.ds != nullptr ? dkdv_s<D, true>(a) : dkdv_s<D, false>(a);
+}
+
+#define VITATTN_DKDV_INSTANTIATE(D, S)                                                                         \
+  template __global__ void attn_bwd_dkdv_kernel<D, S>(                                                        \
+      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
+      const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
+      float* __restrict__, uint16_t* __restrict__, const Map, const Map, const Map, const Map, const Map,      \
+      const Map, int, int, int, int, int, int, float, float);
+VITATTN_DKDV_INSTANTIATE(128, false)
+VITATTN_DKDV_INSTANTIATE(64, false)
+VITATTN_DKDV_INSTANTIATE(96, false)
+VITATTN_DKDV_INSTANTIATE(160, false)
+VITATTN_DKDV_INSTANTIATE(128, true)
+VITATTN_DKDV_INSTANTIATE(64, true)
+VITATTN_DKDV_INSTANTIATE(96, true)
+VITATTN_DKDV_INSTANTIATE(160, true)
+#undef VITATTN_DKDV_INSTANTIATE
+
+template <int D>
+static hipError_t dq_ds_d(const BwdArgs& a) {
+  constexpr int NW = 8;
+  const int n_qt = (a.Nq + 32 * NW - 1) / (32 * NW);
+  const int total = a.BH * n_qt;
+  hipLaunchKernelGGL((attn_bwd_dq_ds_kernel<D, NW>), dim3(total), dim3(64 * NW), 0, a.stream, a.k, a.ds, a.dq, a.mk,
+                     a.mdq, a.H, a.d, a.Nq, a.Nk, n_qt, total, ds_key_blocks(a.Nk), ds_query_blocks(a.Nq), a.scale,
+                     a.accumulate_dq ? 1 : 0);
   return hipGetLastError();
 }
 
-#define VITATTN_DKDV_INSTANTIATE(D)                                                                            \
-  template __global__ void attn_bwd_dkdv_kernel<D>(                                                           \
-      const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
-      const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
-      float* __restrict__, const Map, const Map, const Map, const Map, const Map, const Map, int, int, int, int, \
-      int, int, float, float);
-VITATTN_DKDV_INSTANTIATE(128)
-VITATTN_DKDV_INSTANTIATE(64)
-VITATTN_DKDV_INSTANTIATE(96)
-VITATTN_DKDV_INSTANTIATE(160)
-#undef VITATTN_DKDV_INSTANTIATE
+#define VITATTN_DQDS_INSTANTIATE(D)                                                                         \
+  template __global__ void attn_bwd_dq_ds_kernel<D, 8>(const uint16_t* __restrict__, const uint16_t* __restrict__, \
+                                                       float* __restrict__, const Map, const Map, int, int, int, int, \
+                                                       int, int, int, int, float, int);
+VITATTN_DQDS_INSTANTIATE(64)
+VITATTN_DQDS_INSTANTIATE(96)
+VITATTN_DQDS_INSTANTIATE(128)
+VITATTN_DQDS_INSTANTIATE(160)
+#undef VITATTN_DQDS_INSTANTIATE
 
 template <int D, int NW>
 static hipError_t dq_v(const BwdArgs& a) {
@@ -627,7 +898,16 @@ hipError_t launch_bwd_dkdv(const BwdArgs& a) {
     default: return dkdv_d<160>(a);
   }
 }
+hipError_t launch_bwd_dq_ds(const BwdArgs& a) {
+  switch (tile_width(a.d)) {
+    case 64: return dq_ds_d<64>(a);
+    case 96: return dq_ds_d<96>(a);
+    case 128: return dq_ds_d<128>(a);
+    default: return dq_ds_d<160>(a);
+  }
+}
 hipError_t launch_bwd_dq(const BwdArgs& a) {
+  if (a.ds != nullptr) return launch_bwd_dq_ds(a);
   switch (tile_width(a.d)) {
     case 64: return dq_d<64>(a);
     case 96: return dq_d<96>(a);

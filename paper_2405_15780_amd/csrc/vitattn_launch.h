@@ -43,6 +43,7 @@ struct BwdArgs {
   float* dv;
   float* drow;  // workspace region 0: D = rowsum(dO o O), [BH][Nq]
   float* lse2;  // workspace region 1: LSE * log2(e), [BH][Nq]
+  uint16_t* ds;  // dS mode: workspace region 2 (the dS blocks), else nullptr
   Map mq, mk, mv, mo, mg, mdq, mdk, mdv;  // mg: dout
   int H, BH, Nq, Nk, d;  // query rows and key rows per (b, h); d the head dim
   float scale;
@@ -62,8 +63,16 @@ struct MergeArgs {
 hipError_t launch_fwd(const FwdArgs& a);
 
 // Workspace layout of the backward pass: two fp32 regions of region_floats
-// each (D, then LSE*log2(e)), every region 256-byte aligned.
+// each (D, then LSE*log2(e)), every region 256-byte aligned; in the dS mode a
+// third region holds the dS blocks: 2 KB per 32 keys x 32 queries of every
+// head, key blocks rounded up to the dK/dV kernel's 128 keys and query blocks
+// to its 64-query tiles.
 inline size_t bwd_region_floats(long long rows) { return (size_t)((rows + 63) / 64) * 64; }
+inline int ds_key_blocks(int Nk) { return (Nk + 127) / 128 * 4; }
+inline int ds_query_blocks(int Nq) { return (Nq + 63) / 64 * 2; }
+inline size_t ds_region_bytes(long long BH, int Nq, int Nk) {
+  return (size_t)BH * ds_key_blocks(Nk) * ds_query_blocks(Nq) * 2048;
+}
 
 // Kernel tile variant chosen by an environment variable (for tuning sweeps
 // only; 0 or unset selects the default variant).
@@ -71,7 +80,7 @@ int tuning_variant(const char* env_name);
 // Backward stages; launch_bwd runs all three in order.
 hipError_t launch_bwd_rowdot(const BwdArgs& a);
 hipError_t launch_bwd_dkdv(const BwdArgs& a);
-hipError_t launch_bwd_dq(const BwdArgs& a);
+hipError_t launch_bwd_dq(const BwdArgs& a);  // dQ from stored dS when a.ds is set
 hipError_t launch_bwd(const BwdArgs& a);
 hipError_t launch_merge(const MergeArgs& a);
 

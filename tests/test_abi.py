@@ -183,7 +183,8 @@ def bwd_kv(b, B=1, H=1, Nq=8, Nk=5, d=64, scale=0.125, flags=0, ws_bytes=None, o
 
 
 @pytest.mark.parametrize("kw,expected", [
-    (dict(Nk=0), E_INVAL), (dict(flags=2), E_INVAL), (dict(flags=-1), E_INVAL), (dict(d=168), E_UNSUP),
+    (dict(Nk=0), E_INVAL), (dict(flags=4), E_INVAL), (dict(flags=-1), E_INVAL), (dict(d=168), E_UNSUP),
+    (dict(flags=2), E_WS), (dict(flags=3), E_WS),  # the dS mode needs its larger workspace
     (dict(ws_bytes=1), E_WS), (dict(override={6: None}), E_INVAL), (dict(override={7: 4102}), E_INVAL),
 ])
 def test_bwd_kv_rejects_bad_arguments(kw, expected):
@@ -338,4 +339,34 @@ def test_bwd_strided_output_overlap_and_workspace():
         assert bwd_strided(b, bad=(i, S(576, 0, 72))) == E_INVAL
     assert bwd_strided(b, flags=4) == E_INVAL
     assert bwd_strided(b, ws_bytes=16) == E_WS
+    assert b.untouched()
+
+
+# ------------------------------------------------------------ dS mode
+
+
+def test_ds_mode_workspace_sizes():
+    base = va.workspace_bytes(1, 2, 300, 64)
+    assert va.workspace_bytes_kv(1, 2, 300, 300, 64, 0) == base
+    assert va.workspace_bytes_kv(1, 2, 300, 300, 64, 1) == base
+    # 2 heads x (300 keys -> 3 x 128 -> 12 blocks) x (300 queries -> 5 x 64 -> 10 blocks) x 2 KB
+    assert va.workspace_bytes_kv(1, 2, 300, 300, 64, 2) == base + 2 * 12 * 10 * 2048
+    assert va.workspace_bytes_kv(1, 2, 188416, 188416, 128, 2) > 140e9
+    assert va.workspace_bytes_kv(1, 2, 300, 300, 64, 4) == 0
+    assert va.workspace_bytes_kv(1, 2, 300, 300, 100, 2) == 0
+
+
+def test_ds_mode_stages_validate():
+    b = Bufs()
+    L = lib()
+    need = va.workspace_bytes_kv(1, 1, 8, 8, 64, 2)
+    assert L.vitattn_bwd_dkdv_ds(b.p(0), b.p(1), b.p(2), b.p(3), b.p(4), b.p(5), b.p(6), 1, 1, 8, 64, 0.1, b.p(7),
+                                 need - 1, None) == E_WS
+    assert L.vitattn_bwd_dkdv_ds(b.p(0), b.p(1), b.p(2), None, b.p(4), b.p(5), b.p(6), 1, 1, 8, 64, 0.1, b.p(7),
+                                 need, None) == E_INVAL
+    assert L.vitattn_bwd_dkdv_ds(b.p(0), b.p(1), b.p(2), b.p(3), b.p(4), b.p(5), b.p(6), 1, 1, 8, 100, 0.1, b.p(7),
+                                 need, None) == E_UNSUP
+    assert L.vitattn_bwd_dq_from_ds(b.p(1), b.p(5), 1, 1, 8, 64, 0.1, b.p(7), need - 1, None) == E_WS
+    assert L.vitattn_bwd_dq_from_ds(b.p(1), None, 1, 1, 8, 64, 0.1, b.p(7), need, None) == E_INVAL
+    assert L.vitattn_bwd_dq_from_ds(b.p(1), b.p(5), 1, 1, 8, 64, float("nan"), b.p(7), need, None) == E_INVAL
     assert b.untouched()
