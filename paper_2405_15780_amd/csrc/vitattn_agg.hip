@@ -66,6 +66,71 @@ __device__ __forceinline__ float row_dot(const uint16_t* row, const float* x) {
   return acc;
 }
 
+// a full d-element bf16 row into registers (8 elements per 16-byte piece)
+template <int D>
+__device__ __forceinline__ void row_load(const uint16_t* row, uint4 (&r)[D / 8]) {
+  const uint4* p = reinterpret_cast<const uint4*>(row);
+#pragma unroll
+  for (int t = 0; t < D / 8; ++t) r[t] = p[t];
+}
+
+// dot product of a row held in registers with the fp32 vector x in LDS
+template <int D>
+__device__ __forceinline__ float regs_dot(const uint4 (&r)[D / 8], const float* x) {
+  const float4* xv = reinterpret_cast<const float4*>(x);
+  float acc = 0.f;
+#pragma unroll
+  for (int t = 0; t < D / 8; ++t) {
+    const uint4 w = r[t];
+    const float4 a = xv[2 * t], b = xv[2 * t + 1];
+    acc = fmaf(bf16_lo(w.x), a.x, acc);
+    acc = fmaf(bf16_hi(w.x), a.y, acc);
+    acc = fmaf(bf16_lo(w.y), a.z, acc);
+    acc = fmaf(bf16_hi(w.y), a.w, acc);
+    acc = fmaf(bf16_lo(w.z), b.x, acc);
+    acc = fmaf(bf16_hi(w.z), b.y, acc);
+    acc = fmaf(bf16_lo(w.w), b.z, acc);
+    acc = fmaf(bf16_hi(w.w), b.w, acc);
+  }
+  return acc;
+}
+
+// acc[e] += f * row[e] for a bf16 row held in registers
+template <int D>
+__device__ __forceinline__ void regs_axpy(float f, const uint4 (&r)[D / 8], float (&acc)[D]) {
+#pragma unroll
+  for (int t = 0; t < D / 8; ++t) {
+    const uint4 w = r[t];
+    acc[8 * t + 0] = fmaf(f, bf16_lo(w.x), acc[8 * t + 0]);
+    acc[8 * t + 1] = fmaf(f, bf16_hi(w.x), acc[8 * t + 1]);
+    acc[8 * t + 2] = fmaf(f, bf16_lo(w.y), acc[8 * t + 2]);
+    acc[8 * t + 3] = fmaf(f, bf16_hi(w.y), acc[8 * t + 3]);
+    acc[8 * t + 4] = fmaf(f, bf16_lo(w.z), acc[8 * t + 4]);
+    acc[8 * t + 5] = fmaf(f, bf16_hi(w.z), acc[8 * t + 5]);
+    acc[8 * t + 6] = fmaf(f, bf16_lo(w.w), acc[8 * t + 6]);
+    acc[8 * t + 7] = fmaf(f, bf16_hi(w.w), acc[8 * t + 7]);
+  }
+}
+
+// Sum of a 64-column per-lane vector over the wave's 64 lanes, by recursive
+// halving: at each of six steps a lane keeps half of its columns, receives
+// the partner's (lane ^ o) share of that half and adds; lane l ends with
+// column l's sum (its kept half is the upper one exactly when bit o of l is
+// set, so the surviving column index spells out l). 63 exchanges in all.
+__device__ __forceinline__ float wave_column_sums(float (&acc)[64], int lane) {
+  static_for<0, 6>([&](auto SC) __attribute__((always_inline)) {
+    constexpr int o = 32 >> decltype(SC)::value, half = o;  // columns left: 2*half -> half
+    const bool upper = (lane & o) != 0;
+#pragma unroll
+    for (int i = 0; i < half; ++i) {
+      const float send = upper ? acc[i] : acc[i + half];
+      const float keep = upper ? acc[i + half] : acc[i];
+      acc[i] = keep + __shfl_xor(send, o);
+    }
+  });
+  return acc[0];
+}
+
 // this lane's E = D/64 consecutive columns of a bf16 row, widened
 template <int D>
 __device__ __forceinline__ void row_cols(const uint16_t* row, int lane, float (&out)[D / 64]) {
@@ -148,7 +213,10 @@ __global__ __launch_bounds__(256) void attn_agg_fwd_kernel(const uint16_t* __res
 
 // Block (chunk, h): waves take patches m = chunk*per + w, + 4, ... below
 // (chunk+1)*per and write dk, dv; the block's share of dq_h goes to
-// partial[chunk][h][:].
+// partial[chunk][h][:]. For d = 64 a lane accumulates ds_c k_c of its own
+// keys from the K row it already holds for the score (K is read once), and
+// the wave's columns are summed at the end; wider heads sum dq column-wise
+// from a second, coalesced read of each K row.
 template <int D>
 __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
@@ -165,9 +233,13 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
   __syncthreads();
   const float* qx = qs;
   float* gx = gs[wave];
+  constexpr bool LANE_DQ = D == 64;
   float dq[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) dq[e] = 0.f;
+  float dql[LANE_DQ ? D : 1];  // LANE_DQ: this lane's keys' share of dq, all columns
+#pragma unroll
+  for (int e = 0; e < (LANE_DQ ? D : 1); ++e) dql[e] = 0.f;
   const int m_end = min(M, (chunk + 1) * per);
   for (int m = chunk * per + wave; m < m_end; m += 4) {
     const size_t inst = (size_t)m * H + h;
@@ -190,8 +262,18 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
       const int c = c0 + lane;
       float p = 0.f, ds = 0.f;
       if (c < C) {
-        p = exp2f(row_dot<D>(kb + (size_t)c * D, qx) * c2 - l2);
-        ds = p * (row_dot<D>(vb + (size_t)c * D, gx) - Dm);
+        if constexpr (LANE_DQ) {
+          // dP first, so that only one of the two rows is live at a time
+          const float dp = row_dot<D>(vb + (size_t)c * D, gx);
+          uint4 kr[D / 8];
+          row_load<D>(kb + (size_t)c * D, kr);
+          p = exp2f(regs_dot<D>(kr, qx) * c2 - l2);
+          ds = p * (dp - Dm);
+          regs_axpy<D>(ds, kr, dql);
+        } else {
+          p = exp2f(row_dot<D>(kb + (size_t)c * D, qx) * c2 - l2);
+          ds = p * (row_dot<D>(vb + (size_t)c * D, gx) - Dm);
+        }
       }
       const int n = min(64, C - c0);
       const auto key = [&](int j, const float (&kc)[E]) {
@@ -202,9 +284,14 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
         for (int e = 0; e < E; ++e) {
           dkb[row + lane * E + e] = scale * dsj * qx[lane * E + e];
           dvb[row + lane * E + e] = pj * g[e];
-          dq[e] = fmaf(dsj, kc[e], dq[e]);
+          if constexpr (!LANE_DQ) dq[e] = fmaf(dsj, kc[e], dq[e]);
         }
       };
+      if constexpr (LANE_DQ) {  // stores only: dq came from the registers above
+        const float none[E] = {};
+        for (int j = 0; j < n; ++j) key(j, none);
+        continue;
+      }
       int j = 0;
       for (; j + kAggGroup <= n; j += kAggGroup) {
         float kc[kAggGroup][E];
@@ -220,6 +307,7 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
       }
     }
   }
+  if constexpr (LANE_DQ) dq[0] = wave_column_sums(dql, lane);  // E = 1: lane l holds column l
 #pragma unroll
   for (int e = 0; e < E; ++e) red[wave][lane * E + e] = dq[e];
   __syncthreads();

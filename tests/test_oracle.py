@@ -198,6 +198,46 @@ def test_matches_torch_sdpa_with_autograd():
     np.testing.assert_allclose(r["lse"], lse_t.numpy(), rtol=1e-13)
 
 
+# ------------------------------------------------- the paper's other head dims
+
+
+@pytest.mark.parametrize("d", [72, 160])
+def test_paper_head_dims_closed_forms_and_library_routine(d):
+    """d = 72 (Table I's ViT-10B) and d = 160 (Sec. V-C's model): identical
+    keys give the mean of V and zero dQ, and the whole pass matches torch's
+    SDPA with autograd at these widths."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(20 + d)
+    B, H, N = 1, 2, 29
+    q, v, dout = (rand(rng, B, H, N, d) for _ in range(3))
+    k_same = np.broadcast_to(rand(rng, B, H, 1, d), (B, H, N, d)).copy()
+    s = 1.0 / math.sqrt(d)
+    r = oracle.forward_backward(q, k_same, v, dout, s)
+    np.testing.assert_allclose(r["o"], np.broadcast_to(v.mean(axis=2, keepdims=True), v.shape), atol=1e-13)
+    assert np.abs(r["dq"]).max() < 1e-12
+    k = rand(rng, B, H, N, d)
+    r = oracle.forward_backward(q, k, v, dout, s, block=8)
+    tq, tk, tv = (torch.tensor(x, requires_grad=True) for x in (q, k, v))
+    to = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, scale=A.fp32_scale(s))
+    to.backward(torch.tensor(dout))
+    np.testing.assert_allclose(r["o"], to.detach().numpy(), rtol=1e-11, atol=1e-13)
+    for name, t in (("dq", tq), ("dk", tk), ("dv", tv)):
+        np.testing.assert_allclose(r[name], t.grad.numpy(), rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("d", [72, 160])
+def test_paper_head_dims_match_naive_loops(d):
+    rng = np.random.default_rng(40 + d)
+    N = 6
+    q, k, v, dout = (rand(rng, 1, 1, N, d) for _ in range(4))
+    s = 1.0 / math.sqrt(d)
+    r = oracle.forward_backward(q, k, v, dout, s, block=4)
+    n = oracle.naive.attention_head(q[0, 0].tolist(), k[0, 0].tolist(), v[0, 0].tolist(), A.fp32_scale(s),
+                                    dout[0, 0].tolist())
+    for name in ("o", "lse", "D", "dq", "dk", "dv"):
+        np.testing.assert_allclose(r[name][0, 0], np.array(n[name]), rtol=1e-12, atol=1e-14)
+
+
 # ------------------------------------------------------------ sampled-row paths
 
 
