@@ -62,6 +62,7 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __
 
 constexpr int kDkvBK = 32 * kBwdWaves;  // keys per workgroup
 constexpr int kDkvBQ = 64;              // queries per streamed tile
+constexpr int kDkvAhead = 2;            // LDS operand reads this many matrix-core ops ahead (3 measured no better)
 
 // Direct global -> LDS copy of a tile's row statistics: 64 floats of D and
 // 64 of LSE*log2(e) (one dword per lane; rows past the end read as zeros).
@@ -271,9 +272,10 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     if constexpr (!RP) flush_ds();  // the previous tile's dS, before this tile's DMA requests
     read_side(0);
     if constexpr (!LEAN) read_side(1);
-    bf16x8 aq[3];
-    aq[0] = read_a(0);
-    aq[1] = read_a(1);
+    constexpr int AH = kDkvAhead;  // operand reads run AH ops ahead of their matrix-core op
+    bf16x8 aq[AH + 1];
+#pragma unroll
+    for (int i = 0; i < AH; ++i) aq[i] = read_a(i);
     sched_fence();
     prefetch();
     sched_fence();
@@ -283,14 +285,14 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     static_for<0, NOPS>([&](auto IC) __attribute__((always_inline)) {
       constexpr int i = decltype(IC)::value;
       constexpr int ph = i / PH, j = i % PH, qb = ph & 1;
-      if constexpr (i + 2 < NOPS) aq[(i + 2) % 3] = read_a(i + 2);
+      if constexpr (i + AH < NOPS) aq[(i + AH) % (AH + 1)] = read_a(i + AH);
       if constexpr (ph < 2) {
         if constexpr (j == 0) m1[qb] = zero16();
-        m1[qb] = mfma32(aq[i % 3], hf[j], m1[qb]);
+        m1[qb] = mfma32(aq[i % (AH + 1)], hf[j], m1[qb]);
         if constexpr (ph == 1) valu(0, j);
         if constexpr (LEAN && i == 2 * PH - 1) read_side(1);
       } else {
-        acc[j % NCB] = mfma32(aq[i % 3], ob[qb][j / NCB], acc[j % NCB]);
+        acc[j % NCB] = mfma32(aq[i % (AH + 1)], ob[qb][j / NCB], acc[j % NCB]);
         if constexpr (ph == 2) valu(1, j);
       }
       sched_fence();
@@ -651,7 +653,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
 // it (lane j of a 16-lane group supplies the address of the 4 consecutive
 // queries of key 16 ks + 4 h + j/4, so result lane i gets query i's entry of
 // 4 consecutive keys).
-template <int D, int NW>
+template <int D, int NW, int RING>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ ds, float* __restrict__ dq, const Map mk,
     const Map mdq, int H, int dr, int Nq, int Nk, int n_qtiles, int total, int nkb, int nqb, float scale,
@@ -660,7 +662,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
   constexpr int NCB = D / 32;
   constexpr int KTILE = BN * D * 2;  // bytes of a K tile
   constexpr int STILE = NW * 2048;   // bytes of the dS blocks of a tile
-  constexpr int RING = 6;
+  static_assert(RING == 4 || RING == 6, "ring depth");
   __shared__ __attribute__((aligned(1024))) char kbuf0[KTILE];
   __shared__ __attribute__((aligned(1024))) char kbuf1[KTILE];
   __shared__ __attribute__((aligned(1024))) char kbuf2[KTILE];
@@ -673,8 +675,9 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
   __shared__ __attribute__((aligned(1024))) char sbuf3[STILE];
   __shared__ __attribute__((aligned(1024))) char sbuf4[STILE];
   __shared__ __attribute__((aligned(1024))) char sbuf5[STILE];
-  char* const kbuf[RING] = {kbuf0, kbuf1, kbuf2, kbuf3, kbuf4, kbuf5};
-  char* const sbuf[RING] = {sbuf0, sbuf1, sbuf2, sbuf3, sbuf4, sbuf5};
+  // (a ring of four leaves the last two slot pairs unreferenced, and unallocated)
+  char* const kbuf[6] = {kbuf0, kbuf1, kbuf2, kbuf3, RING > 4 ? kbuf4 : kbuf0, RING > 4 ? kbuf5 : kbuf1};
+  char* const sbuf[6] = {sbuf0, sbuf1, sbuf2, sbuf3, RING > 4 ? sbuf4 : sbuf0, RING > 4 ? sbuf5 : sbuf1};
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;
@@ -763,8 +766,10 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
     stage(S1{}, jj + 1);
     stage(S2{}, jj + 2);
     stage(S3{}, jj + 3);
-    stage(S4{}, jj + 4);
-    stage(S5{}, jj + 5);
+    if constexpr (RING > 4) {
+      stage(S4{}, jj + 4);
+      stage(S5{}, jj + 5);
+    }
   }
   wait_vmem();  // requests past the last tile must land before this LDS is reassigned
 
@@ -830,25 +835,30 @@ VITATTN_DKDV_INSTANTIATE(96, true)
 VITATTN_DKDV_INSTANTIATE(160, true)
 #undef VITATTN_DKDV_INSTANTIATE
 
-template <int D>
-static hipError_t dq_ds_d(const BwdArgs& a) {
-  constexpr int NW = 8;
+template <int D, int NW, int RING>
+static hipError_t dq_ds_v(const BwdArgs& a) {
   const int n_qt = (a.Nq + 32 * NW - 1) / (32 * NW);
   const int total = a.BH * n_qt;
-  hipLaunchKernelGGL((attn_bwd_dq_ds_kernel<D, NW>), dim3(total), dim3(64 * NW), 0, a.stream, a.k, a.ds, a.dq, a.mk,
-                     a.mdq, a.H, a.d, a.Nq, a.Nk, n_qt, total, ds_key_blocks(a.Nk), ds_query_blocks(a.Nq), a.scale,
-                     a.accumulate_dq ? 1 : 0);
+  hipLaunchKernelGGL((attn_bwd_dq_ds_kernel<D, NW, RING>), dim3(total), dim3(64 * NW), 0, a.stream, a.k, a.ds, a.dq,
+                     a.mk, a.mdq, a.H, a.d, a.Nq, a.Nk, n_qt, total, ds_key_blocks(a.Nk), ds_query_blocks(a.Nq),
+                     a.scale, a.accumulate_dq ? 1 : 0);
   return hipGetLastError();
 }
+// 8 waves and a six-slot ring measured best (6.1 TB/s at N = 188,416 against
+// 4.9 for 4 waves with two workgroups per CU and 6.0 for a four-slot ring)
+template <int D>
+static hipError_t dq_ds_d(const BwdArgs& a) {
+  return dq_ds_v<D, 8, 6>(a);
+}
 
-#define VITATTN_DQDS_INSTANTIATE(D)                                                                         \
-  template __global__ void attn_bwd_dq_ds_kernel<D, 8>(const uint16_t* __restrict__, const uint16_t* __restrict__, \
-                                                       float* __restrict__, const Map, const Map, int, int, int, int, \
-                                                       int, int, int, int, float, int);
-VITATTN_DQDS_INSTANTIATE(64)
-VITATTN_DQDS_INSTANTIATE(96)
-VITATTN_DQDS_INSTANTIATE(128)
-VITATTN_DQDS_INSTANTIATE(160)
+#define VITATTN_DQDS_INSTANTIATE(D, NW, R)                                                                    \
+  template __global__ void attn_bwd_dq_ds_kernel<D, NW, R>(                                                   \
+      const uint16_t* __restrict__, const uint16_t* __restrict__, float* __restrict__, const Map, const Map, int, \
+      int, int, int, int, int, int, int, float, int);
+VITATTN_DQDS_INSTANTIATE(64, 8, 6)
+VITATTN_DQDS_INSTANTIATE(96, 8, 6)
+VITATTN_DQDS_INSTANTIATE(128, 8, 6)
+VITATTN_DQDS_INSTANTIATE(160, 8, 6)
 #undef VITATTN_DQDS_INSTANTIATE
 
 template <int D, int NW>
