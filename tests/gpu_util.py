@@ -23,7 +23,9 @@ def to_device(bits):
     return t.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(t.bfloat16).cuda()
 
 
-def run_hip(x, scale, backward=True):
+def run_hip(x, scale, backward=True, store_ds=False):
+    """Forward (and backward) through the binding; store_ds selects the
+    backward's dS mode (dQ from stored dS), whose workspace is freed again."""
     import paper_2405_15780_amd as va
 
     t = torch()
@@ -31,9 +33,11 @@ def run_hip(x, scale, backward=True):
     o, lse = va.fwd(dev["q"], dev["k"], dev["v"], scale)
     res = {"o": o, "lse": lse}
     if backward:
-        dq, dk, dv = va.bwd(dev["q"], dev["k"], dev["v"], o, lse, dev["dout"], scale)
+        dq, dk, dv = va.bwd(dev["q"], dev["k"], dev["v"], o, lse, dev["dout"], scale, store_ds=store_ds)
         res.update(dq=dq, dk=dk, dv=dv)
     t.cuda.synchronize()
+    if store_ds:
+        t.cuda.empty_cache()
     return res
 
 

@@ -97,12 +97,15 @@ def test_config2_full_heads_sampled_rows_and_identities():
     _identities(w, x, res)
 
 
+@pytest.mark.parametrize("store_ds", [False, True], ids=["recompute", "stored-ds"])
 @pytest.mark.parametrize("cid", [3, 4])
-def test_long_sequence_configs_sampled(cid):
+def test_long_sequence_configs_sampled(cid, store_ds):
+    """Configs 3 and 4 at full size in both backward modes (the benchmark times
+    config 4 with the dS mode when its workspace fits)."""
     w = workloads.CONFIGS[cid]
-    print(f"config {cid}: generating inputs", flush=True)
+    print(f"config {cid} ({'stored-ds' if store_ds else 'recompute'} backward): generating inputs", flush=True)
     x = workloads.make_inputs(w)
-    res = run_hip(x, w.scale)
+    res = run_hip(x, w.scale, store_ds=store_ds)
     _sampled_query_check(w, x, res, with_grad=True)
     path = os.path.join(GOLDEN, f"sampled_grads_c{cid}.npz")
     gold = np.load(path)
