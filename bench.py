@@ -45,6 +45,8 @@ def parse():
     p.add_argument("--bwd-mode", choices=["auto", "recompute", "stored-ds"], default="auto",
                    help="backward pass of the default workload: recompute S and dP for dQ, or dQ from the dS "
                         "blocks the dK/dV kernel stores (a B*H*N^2*2-byte workspace); auto = stored-ds when it fits")
+    p.add_argument("--hbm-reference", action="store_true",
+                   help="only measure the streaming rate of a plain elementwise kernel over 8 GiB")
     p.add_argument("--no-compare", action="store_true",
                    help="skip timing the other backward mode after the timed region (for profiler runs)")
     p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg", "d72", "d160", "bnhd"],
@@ -113,6 +115,29 @@ def copy_calibration():
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 3}), flush=True)
+
+
+def hbm_reference():
+    """Practical HBM streaming rate on this GPU: an elementwise torch kernel
+    (read one fp32 array, write another) over 8 GiB, the ceiling that the
+    HBM-bound kernels here are compared with besides the 8 TB/s datasheet peak."""
+    import torch
+
+    n = (8 << 30) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        torch.add(a, 1.0, out=b)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        torch.add(a, 1.0, out=b)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 10
+    print(json.dumps({"hbm_reference": "torch.add over 8 GiB fp32 (read + write)", "ms": ms,
+                      "GB_s": 2 * n * 4 / ms / 1e6, "frac_of_8TBs": 2 * n * 4 / ms / 1e6 / PEAK_HBM_GBS}), flush=True)
 
 
 class SmiSampler:
@@ -466,6 +491,9 @@ def main():
     args = parse()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.hbm_reference:
+        hbm_reference()
         return
     if args.row in ATT_ROWS:
         if args.gpus != 1:
