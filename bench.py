@@ -497,18 +497,18 @@ def main():
         return
     if args.row in ATT_ROWS:
         if args.gpus != 1:
-            print(json.dumps({"error": "this build runs on one GPU only", "n_gpus": args.gpus}))
+            print(json.dumps({"error": "one GPU per run: the library has no multi-GPU path; use --gpus 1", "n_gpus": args.gpus}))
             sys.exit(2)
         bench_attention_row(args)
         return
     if args.row != "attention":
         if args.gpus != 1:
-            print(json.dumps({"error": "this build runs on one GPU only", "n_gpus": args.gpus}))
+            print(json.dumps({"error": "one GPU per run: the library has no multi-GPU path; use --gpus 1", "n_gpus": args.gpus}))
             sys.exit(2)
         bench_row(args)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
+        print(json.dumps({"error": "one GPU per run: the library has no multi-GPU path; use --gpus 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
 
