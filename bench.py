@@ -47,6 +47,9 @@ def parse():
                         "blocks the dK/dV kernel stores (a B*H*N^2*2-byte workspace); auto = stored-ds when it fits")
     p.add_argument("--hbm-reference", action="store_true",
                    help="only measure the streaming rate of a plain elementwise kernel over 8 GiB")
+    p.add_argument("--mfma-reference", action="store_true",
+                   help="only measure the library bf16 GEMM (torch.matmul, 16384^3) on random normal and on "
+                        "zero operands, with the clock and power it runs at")
     p.add_argument("--no-compare", action="store_true",
                    help="skip timing the other backward mode after the timed region (for profiler runs)")
     p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg", "d72", "d160", "bnhd"],
@@ -138,6 +141,46 @@ def hbm_reference():
     ms = e0.elapsed_time(e1) / 10
     print(json.dumps({"hbm_reference": "torch.add over 8 GiB fp32 (read + write)", "ms": ms,
                       "GB_s": 2 * n * 4 / ms / 1e6, "frac_of_8TBs": 2 * n * 4 / ms / 1e6 / PEAK_HBM_GBS}), flush=True)
+
+
+def vendor_gemm_tflops(x, y, reps):
+    """Mean rate of torch.matmul (hipBLASLt) on two square bf16 operands."""
+    import torch
+
+    n = x.shape[0]
+    c = x @ y
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        c = x @ y
+    e1.record()
+    torch.cuda.synchronize()
+    del c
+    ms = e0.elapsed_time(e1) / reps
+    return ms, 2 * n**3 / ms / 1e9
+
+
+def mfma_reference():
+    """Practical bf16 matrix-core rate on this GPU: the vendor GEMM
+    (torch.matmul, which calls hipBLASLt) on 16384^3 bf16 operands, first
+    random normal (the bit activity of real activations), then all zeros. The
+    dense 2.5 PF/s peak assumes the 2.4 GHz peak clock; under a sustained MFMA
+    load the board power limit lowers the clock, and more so the more operand
+    bits toggle, so the random-operand rate is the ceiling that the attention
+    kernels are compared with besides the datasheet peak."""
+    import torch
+
+    n = 16384
+    out = {"mfma_reference": "torch.matmul bf16 16384^3", "peak_tflops": PEAK_BF16_TFLOPS}
+    a = torch.randn(n, n, device="cuda:0").to(torch.bfloat16)
+    b = torch.randn(n, n, device="cuda:0").to(torch.bfloat16)
+    z = torch.zeros_like(a)
+    for name, x, y in (("random_normal", a, b), ("zeros", z, z)):
+        with SmiSampler() as smi:
+            ms, tf = vendor_gemm_tflops(x, y, 300)
+        out[name] = {"ms": ms, "tflops": tf, "frac_of_peak": tf / PEAK_BF16_TFLOPS, "smi": smi.summary()}
+    print(json.dumps(out), flush=True)
 
 
 class SmiSampler:
@@ -495,6 +538,9 @@ def main():
     if args.hbm_reference:
         hbm_reference()
         return
+    if args.mfma_reference:
+        mfma_reference()
+        return
     if args.row in ATT_ROWS:
         if args.gpus != 1:
             print(json.dumps({"error": "one GPU per run: the library has no multi-GPU path; use --gpus 1", "n_gpus": args.gpus}))
@@ -638,6 +684,18 @@ def main():
                "kernels_ms": {n: float(np.mean([e[spans[n][0]].elapsed_time(e[spans[n][1]]) for e in ev2]))
                               for n in names}}
 
+    # the vendor bf16 GEMM on random operands in the same process, after the
+    # timed region: the power-limited rate that dense matrix-core work reaches
+    ceiling = None
+    if not args.no_compare:
+        g = torch.Generator(device="cuda:0").manual_seed(w.seed)
+        ga, gb = (torch.randn(16384, 16384, device="cuda:0", generator=g).to(torch.bfloat16) for _ in range(2))
+        g_ms, g_tf = vendor_gemm_tflops(ga, gb, 60)
+        del ga, gb
+        ceiling = {"kind": "torch.matmul bf16 16384^3, random normal operands", "tflops": g_tf,
+                   "value_frac": value / g_tf,
+                   "kernel_frac": {n: per_kernel[n]["tflops"] / g_tf for n in names if "tflops" in per_kernel[n]}}
+
     smi_summary = smi.summary()
     clock = None
     if smi_summary:
@@ -667,6 +725,7 @@ def main():
         "step_ms_min": float(np.min(step_ms)),
         "clock": clock,
         "kernels": per_kernel,
+        "practical_ceiling": ceiling,
         "wall_s_timed": wall,
         "roofline": roof,
         "kernel_sources": kernel_sources_digest(args.row),
