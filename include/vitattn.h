@@ -296,7 +296,8 @@ int vitattn_ulysses_unpack_out(const void* recv, void* x, int B, int Nl, int H, 
 int vitattn_agg_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int M, int H, int C, int d,
                     float scale, void* stream);
 
-/* Workspace bytes of vitattn_agg_bwd (per-block dq partials); 0 for invalid sizes. */
+/* Workspace bytes of vitattn_agg_bwd: dq partials, one per head and group of four
+ * patches (ceil(M/4) x H x d floats); 0 for invalid sizes. */
 size_t vitattn_agg_bwd_workspace_bytes(int M, int H, int C, int d);
 
 /* o and lse are vitattn_agg_fwd's outputs for the same q, k, v; workspace is

@@ -89,13 +89,6 @@ vitattn_strides dense(int H, int N, int d) {
 
 }  // namespace
 
-namespace vitattn {
-int tuning_variant(const char* env_name) {
-  const char* s = getenv(env_name);
-  return s ? atoi(s) : 0;
-}
-}  // namespace vitattn
-
 extern "C" {
 
 const char* vitattn_status_str(int status) {
@@ -401,7 +394,7 @@ static int check_agg(int M, int H, int C, int d, float scale) {
 
 size_t vitattn_agg_bwd_workspace_bytes(int M, int H, int C, int d) {
   if (check_agg(M, H, C, d, 1.f) != VITATTN_OK) return 0;
-  return (size_t)vitattn::agg_chunks(M, H) * H * d * sizeof(float);
+  return (size_t)vitattn::agg_partials(M) * H * d * sizeof(float);
 }
 
 int vitattn_agg_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int M, int H, int C, int d,

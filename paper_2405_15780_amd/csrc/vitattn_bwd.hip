@@ -876,25 +876,11 @@ static hipError_t dq_v(const BwdArgs& a) {
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
       const Map, const Map, const Map, const Map, const Map, int, int, int, int, int, int, float, float, int);
-VITATTN_DQ_INSTANTIATE(128, 4)
 VITATTN_DQ_INSTANTIATE(128, 8)
-VITATTN_DQ_INSTANTIATE(64, 4)
 VITATTN_DQ_INSTANTIATE(64, 8)
 VITATTN_DQ_INSTANTIATE(96, 8)
 VITATTN_DQ_INSTANTIATE(160, 8)
 #undef VITATTN_DQ_INSTANTIATE
-
-template <int D>
-static hipError_t dq_d(const BwdArgs& a) {
-  if constexpr (D == 64 || D == 128) {
-    switch (tuning_variant("VITATTN_DQ_VARIANT")) {
-      case 1: return dq_v<D, 4>(a);
-      default: return dq_v<D, 8>(a);
-    }
-  } else {
-    return dq_v<D, 8>(a);
-  }
-}
 
 hipError_t launch_bwd_rowdot(const BwdArgs& a) {
   const int chunks = a.d / 8;
@@ -919,10 +905,10 @@ hipError_t launch_bwd_dq_ds(const BwdArgs& a) {
 hipError_t launch_bwd_dq(const BwdArgs& a) {
   if (a.ds != nullptr) return launch_bwd_dq_ds(a);
   switch (tile_width(a.d)) {
-    case 64: return dq_d<64>(a);
-    case 96: return dq_d<96>(a);
-    case 128: return dq_d<128>(a);
-    default: return dq_d<160>(a);
+    case 64: return dq_v<64, 8>(a);
+    case 96: return dq_v<96, 8>(a);
+    case 128: return dq_v<128, 8>(a);
+    default: return dq_v<160, 8>(a);
   }
 }
 

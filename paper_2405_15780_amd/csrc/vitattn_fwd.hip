@@ -326,9 +326,7 @@ static hipError_t launch_fwd_v(const FwdArgs& a) {
 // Every tile variant is instantiated explicitly: hipcc otherwise omits the
 // host-side launch stub of some instantiations reached only through this
 // dispatch, and the library then fails to load.
-#define VITATTN_FWD_VARIANTS(X)                                                                     \
-  X(128, 2, 8, 2) X(128, 2, 4, 2) X(128, 1, 8, 2) X(64, 2, 8, 2) X(64, 2, 4, 2) X(64, 1, 8, 2) X(96, 2, 8, 2) \
-      X(160, 1, 8, 2)
+#define VITATTN_FWD_VARIANTS(X) X(128, 2, 8, 2) X(64, 2, 8, 2) X(96, 2, 8, 2) X(160, 1, 8, 2)
 #define VITATTN_FWD_INSTANTIATE(D, KB, NW, MINW)                                                               \
   template __global__ void attn_fwd_kernel<D, KB, NW, MINW>(                                                  \
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
@@ -337,24 +335,14 @@ static hipError_t launch_fwd_v(const FwdArgs& a) {
 VITATTN_FWD_VARIANTS(VITATTN_FWD_INSTANTIATE)
 #undef VITATTN_FWD_INSTANTIATE
 
-// Tile variants (key blocks per tile, waves per workgroup, waves per SIMD);
-// 0 is the default.
-template <int D>
-static hipError_t launch_fwd_d(const FwdArgs& a, int variant) {
-  switch (variant) {
-    case 1: return launch_fwd_v<D, 2, 8, 2>(a);
-    case 2: return launch_fwd_v<D, 2, 4, 2>(a);
-    case 3: return launch_fwd_v<D, 1, 8, 2>(a);
-    default: return launch_fwd_v<D, 2, 8, 2>(a);
-  }
-}
-
+// Tile shape per width (key blocks per tile, waves per workgroup, waves per
+// SIMD): two 32-key blocks per tile and 8 waves x 32 queries, except at
+// D = 160, where one key block per tile keeps the registers within budget.
 hipError_t launch_fwd(const FwdArgs& a) {
-  const int variant = tuning_variant("VITATTN_FWD_VARIANT");
   switch (tile_width(a.d)) {
-    case 64: return launch_fwd_d<64>(a, variant);
+    case 64: return launch_fwd_v<64, 2, 8, 2>(a);
     case 96: return launch_fwd_v<96, 2, 8, 2>(a);
-    case 128: return launch_fwd_d<128>(a, variant);
+    case 128: return launch_fwd_v<128, 2, 8, 2>(a);
     default: return launch_fwd_v<160, 1, 8, 2>(a);
   }
 }

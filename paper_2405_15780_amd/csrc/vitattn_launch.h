@@ -74,9 +74,6 @@ inline size_t ds_region_bytes(long long BH, int Nq, int Nk) {
   return (size_t)BH * ds_key_blocks(Nk) * ds_query_blocks(Nq) * 2048;
 }
 
-// Kernel tile variant chosen by an environment variable (for tuning sweeps
-// only; 0 or unset selects the default variant).
-int tuning_variant(const char* env_name);
 // Backward stages; launch_bwd runs all three in order.
 hipError_t launch_bwd_rowdot(const BwdArgs& a);
 hipError_t launch_bwd_dkdv(const BwdArgs& a);
@@ -97,9 +94,7 @@ long ulysses_blocks(int Nl, int H, int row_bytes);  // grid.x of the layout kern
 
 // Channel aggregation (attention of one learnable query per head over the C
 // channel tokens of each of M patches); see vitattn_agg.hip.
-constexpr int kAggMaxChunks = 1024;      // most blocks along M in the backward pass (dq partials)
-constexpr int kAggTargetBlocks = 8192;  // backward blocks (chunks x heads) aimed for
-constexpr int kAggGroup = 16;           // keys whose rows one wave loads together
+constexpr int kAggChunkGroup = 12;  // 1 KB chunks of a [C][d] block whose loads one wave issues together
 struct AggArgs {
   const uint16_t* q;     // [H][d]
   const uint16_t* k;     // [M][H][C][d]
@@ -112,12 +107,12 @@ struct AggArgs {
   float* dq;             // [H][d]
   float* dk;             // [M][H][C][d]
   float* dv;             // [M][H][C][d]
-  float* partial;        // workspace: [chunks][H][d]
+  float* partial;        // workspace: [agg_partials(M)][H][d]
   int M, H, C, d;
   float scale;
   hipStream_t stream;
 };
-int agg_chunks(int M, int H);
+int agg_partials(int M);  // dq partials of the backward pass
 hipError_t launch_agg_fwd(const AggArgs& a);
 hipError_t launch_agg_bwd(const AggArgs& a);
 

@@ -253,8 +253,9 @@ def test_agg_bwd_validates_workspace_and_pointers():
     b = Bufs()
     L = lib()
     wsb = L.vitattn_agg_bwd_workspace_bytes(3, 2, 5, 64)
-    assert wsb == 3 * 2 * 64 * 4
-    assert L.vitattn_agg_bwd_workspace_bytes(5000, 2, 5, 64) == 1024 * 2 * 64 * 4
+    assert wsb == 1 * 2 * 64 * 4  # one group of four patches
+    assert L.vitattn_agg_bwd_workspace_bytes(5000, 2, 5, 64) == 1250 * 2 * 64 * 4
+    assert L.vitattn_agg_bwd_workspace_bytes(5001, 2, 5, 64) == 1251 * 2 * 64 * 4
     assert L.vitattn_agg_bwd_workspace_bytes(0, 2, 5, 64) == 0
     ptrs = [b.p(i) for i in range(9)]
     assert L.vitattn_agg_bwd(*ptrs, 3, 2, 5, 64, 0.1, b.p(9), wsb - 4, None) == E_WS
