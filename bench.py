@@ -193,6 +193,11 @@ class SmiSampler:
         import threading
 
         self.exe = shutil.which("amd-smi")
+        # Under a profiler its preloaded library would start in the amd-smi
+        # child too and bring up the GPU there before that launcher replaces
+        # itself with python: never sample while profiled.
+        if "rocprof" in os.environ.get("LD_PRELOAD", "") or any(k.startswith("ROCPROF") for k in os.environ):
+            self.exe = None
         self.samples = []
         self._stop = threading.Event()
         self._thread = threading.Thread(target=self._run, daemon=True)
