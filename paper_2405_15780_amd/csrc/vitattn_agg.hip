@@ -250,24 +250,25 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
 }
 
 // dq[t] = scale * the sum over patch groups of partial[group][t], t = h*D + e.
-// A block takes 16 columns; its thread (r, col) sums groups r, r+16, r+32,
-// ... in that order, then thread (0, col) adds the 16 sums in order of r.
-__global__ __launch_bounds__(256) void attn_agg_dq_kernel(const float* __restrict__ partial, float* __restrict__ dq,
-                                                          int groups, int HD, float scale) {
-  __shared__ float red[16][17];
+// A block of 1,024 threads takes 16 columns; its thread (r, col) sums groups
+// r, r+64, r+128, ... in that order, then thread (0, col) adds the 64 sums in
+// order of r.
+__global__ __launch_bounds__(1024) void attn_agg_dq_kernel(const float* __restrict__ partial, float* __restrict__ dq,
+                                                           int groups, int HD, float scale) {
+  __shared__ float red[64][17];
   const int col = threadIdx.x & 15, r = threadIdx.x >> 4;
   const int t = blockIdx.x * 16 + col;
   float s = 0.f;
   if (t < HD) {
 #pragma unroll 8
-    for (int c = r; c < groups; c += 16) s += partial[(size_t)c * HD + t];
+    for (int c = r; c < groups; c += 64) s += partial[(size_t)c * HD + t];
   }
   red[r][col] = s;
   __syncthreads();
   if (r == 0 && t < HD) {
     float tot = 0.f;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) tot += red[i][col];
+    for (int i = 0; i < 64; ++i) tot += red[i][col];
     dq[t] = scale * tot;
   }
 }
@@ -303,7 +304,7 @@ static hipError_t agg_bwd_d(const AggArgs& a) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int HD = a.H * D;
-  hipLaunchKernelGGL(attn_agg_dq_kernel, dim3((unsigned)((HD + 15) / 16)), dim3(256), 0, a.stream, a.partial, a.dq,
+  hipLaunchKernelGGL(attn_agg_dq_kernel, dim3((unsigned)((HD + 15) / 16)), dim3(1024), 0, a.stream, a.partial, a.dq,
                      parts, HD, a.scale);
   return hipGetLastError();
 }
