@@ -46,7 +46,8 @@ def parse():
                    help="backward pass of the default workload: recompute S and dP for dQ, or dQ from the dS "
                         "blocks the dK/dV kernel stores (a B*H*N^2*2-byte workspace); auto = stored-ds when it fits")
     p.add_argument("--hbm-reference", action="store_true",
-                   help="only measure the streaming rate of a plain elementwise kernel over 8 GiB")
+                   help="only measure the streaming rates of plain elementwise kernels (read+write, "
+                        "read 1 : write 2, write only)")
     p.add_argument("--mfma-reference", action="store_true",
                    help="only measure the library bf16 GEMM (torch.matmul, 16384^3) on random normal and on "
                         "zero operands, with the clock and power it runs at")
@@ -121,26 +122,44 @@ def copy_calibration():
 
 
 def hbm_reference():
-    """Practical HBM streaming rate on this GPU: an elementwise torch kernel
-    (read one fp32 array, write another) over 8 GiB, the ceiling that the
-    HBM-bound kernels here are compared with besides the 8 TB/s datasheet peak."""
+    """Practical HBM streaming rates on this GPU: elementwise torch kernels
+    over GiB-sized arrays, the ceilings that the HBM-bound kernels here are
+    compared with besides the 8 TB/s datasheet peak. Three mixes: read and
+    write equal bytes (fp32 add over 8 GiB), write twice what is read (a
+    bf16 -> fp32 conversion copy, 3 GiB in, 6 GiB out: the aggregation
+    backward's mix) and write only (fp32 fill over 6 GiB)."""
     import torch
 
+    def timed(fn, reps=10):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    out = {"hbm_reference": "plain torch elementwise kernels", "peak_GB_s": PEAK_HBM_GBS}
     n = (8 << 30) // 4
     a = torch.ones(n, dtype=torch.float32, device="cuda:0")
     b = torch.empty_like(a)
-    for _ in range(3):
-        torch.add(a, 1.0, out=b)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(10):
-        torch.add(a, 1.0, out=b)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / 10
-    print(json.dumps({"hbm_reference": "torch.add over 8 GiB fp32 (read + write)", "ms": ms,
-                      "GB_s": 2 * n * 4 / ms / 1e6, "frac_of_8TBs": 2 * n * 4 / ms / 1e6 / PEAK_HBM_GBS}), flush=True)
+    ms = timed(lambda: torch.add(a, 1.0, out=b))
+    out["add_fp32_read1_write1"] = {"bytes": 2 * n * 4, "ms": ms, "GB_s": 2 * n * 4 / ms / 1e6}
+    del a, b
+    n = 1536 << 20
+    a = torch.ones(n, dtype=torch.bfloat16, device="cuda:0")
+    b = torch.empty(n, dtype=torch.float32, device="cuda:0")
+    ms = timed(lambda: b.copy_(a))
+    out["convert_bf16_to_fp32_read1_write2"] = {"bytes": 6 * n, "ms": ms, "GB_s": 6 * n / ms / 1e6}
+    ms = timed(lambda: b.fill_(1.0))
+    out["fill_fp32_write_only"] = {"bytes": 4 * n, "ms": ms, "GB_s": 4 * n / ms / 1e6}
+    for v in out.values():
+        if isinstance(v, dict):
+            v["frac_of_8TBs"] = v["GB_s"] / PEAK_HBM_GBS
+    print(json.dumps(out), flush=True)
 
 
 def vendor_gemm_tflops(x, y, reps):
