@@ -105,12 +105,36 @@ def _stream_ptr(t) -> int:
     return torch.cuda.current_stream(t.device).cuda_stream
 
 
-def _as_input(t, name):
+def _as_input(t, name, device=None):
     torch = _torch()
-    if not (t.is_cuda and t.dtype == torch.bfloat16 and t.dim() == 4 and (t.shape[3] == 1 or t.stride(3) == 1)):
-        raise TypeError(f"{name} must be a 4-D bfloat16 CUDA tensor [B, H, N, d] with unit stride along d "
-                        "(other strides are free, e.g. a [B, N, H, d] tensor passed as .transpose(1, 2))")
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.bfloat16 and t.dim() == 4
+            and (t.shape[3] == 1 or t.stride(3) == 1) and (device is None or t.device == device)):
+        raise TypeError(f"{name} must be a 4-D bfloat16 CUDA tensor [B, H, N, d] with unit stride along d, on the "
+                        "device of q (other strides are free, e.g. a [B, N, H, d] tensor passed as .transpose(1, 2))")
     return t
+
+
+def _expect(t, name, dtype, shape, device, dense=False):
+    """Raise TypeError unless t is a CUDA tensor of this dtype and exact shape
+    on `device`, with unit stride along its last dim (contiguous if dense).
+    A mismatch would otherwise become an out-of-bounds access on the GPU."""
+    torch = _torch()
+    shape = tuple(int(n) for n in shape)
+    ok = (isinstance(t, torch.Tensor) and t.is_cuda and t.device == device and t.dtype == dtype
+          and tuple(t.shape) == shape)
+    if ok:
+        ok = t.is_contiguous() if dense else (shape[-1] == 1 or t.stride(-1) == 1)
+    if not ok:
+        layout = "contiguous" if dense else "unit stride along the last dim"
+        raise TypeError(f"{name} must be a {dtype} CUDA tensor of shape {shape} on {device} ({layout})")
+    return t
+
+
+def _expect_workspace(ws, device):
+    torch = _torch()
+    if not (isinstance(ws, torch.Tensor) and ws.is_cuda and ws.device == device and ws.is_contiguous()):
+        raise TypeError(f"workspace must be a contiguous CUDA tensor on {device}")
+    return ws
 
 
 def strides_of(t):
@@ -146,14 +170,17 @@ def fwd(q, k, v, scale=None, out=None):
     """O (fp32 [B,H,Nq,d]) and LSE (fp32 [B,H,Nq]) of softmax(scale Q K^T) V;
     k and v may hold a different number of rows Nk (one key segment)."""
     torch = _torch()
-    for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _as_input(t, n)
+    _as_input(q, "q")
+    for t, n in ((k, "k"), (v, "v")):
+        _as_input(t, n, q.device)
     B, H, Nq, Nk, d = _kv_shapes(q, k, v)
     if out is None:
         o = torch.empty((B, H, Nq, d), dtype=torch.float32, device=q.device)
         lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
     else:
         o, lse = out
+        _expect(o, "o", torch.float32, (B, H, Nq, d), q.device)
+        _expect(lse, "lse", torch.float32, (B, H, Nq), q.device, dense=True)
     lib = library()
     if not _dense(q, k, v, o):
         st = lib.vitattn_fwd_strided(q.data_ptr(), strides_of(q), k.data_ptr(), strides_of(k), v.data_ptr(),
@@ -175,6 +202,7 @@ def _workspace(q, k, workspace, flags=0):
     need = workspace_bytes_kv(B, H, N, k.shape[2], d, flags)
     if workspace is None:
         workspace = torch.empty(max(need, 4) // 4, dtype=torch.float32, device=q.device)
+    _expect_workspace(workspace, q.device)
     return workspace, workspace.numel() * workspace.element_size()
 
 
@@ -185,9 +213,13 @@ def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None, accumulate_
     store_ds selects the dS mode (dQ from stored dS; a workspace of about
     B*H*Nq*Nk*2 bytes, see workspace_bytes_kv)."""
     torch = _torch()
-    for t, n in ((q, "q"), (k, "k"), (v, "v"), (dout, "dout")):
-        _as_input(t, n)
+    _as_input(q, "q")
+    for t, n in ((k, "k"), (v, "v"), (dout, "dout")):
+        _as_input(t, n, q.device)
     B, H, Nq, Nk, d = _kv_shapes(q, k, v)
+    _expect(dout, "dout", torch.bfloat16, (B, H, Nq, d), q.device)
+    _expect(o, "o", torch.float32, (B, H, Nq, d), q.device)
+    _expect(lse, "lse", torch.float32, (B, H, Nq), q.device, dense=True)
     flags = (VITATTN_BWD_ACCUMULATE_DQ if accumulate_dq else 0) | (VITATTN_BWD_STORE_DS if store_ds else 0)
     ws, ws_bytes = _workspace(q, k, workspace, flags)
     if out is None:
@@ -197,6 +229,9 @@ def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None, accumulate_
         dk, dv = (torch.empty((B, H, Nk, d), dtype=torch.float32, device=q.device) for _ in range(2))
     else:
         dq, dk, dv = out
+        _expect(dq, "dq", torch.float32, (B, H, Nq, d), q.device)
+        _expect(dk, "dk", torch.float32, (B, H, Nk, d), q.device)
+        _expect(dv, "dv", torch.float32, (B, H, Nk, d), q.device)
     lib = library()
     if not _dense(q, k, v, o, dout, dq, dk, dv):
         st = lib.vitattn_bwd_strided(q.data_ptr(), strides_of(q), k.data_ptr(), strides_of(k), v.data_ptr(),
@@ -223,34 +258,51 @@ def merge(o_parts, lse_parts, out=None):
     if not (o_parts.is_cuda and o_parts.dtype == torch.float32 and o_parts.dim() == 5 and o_parts.is_contiguous()):
         raise TypeError("o_parts must be a contiguous 5-D float32 CUDA tensor [P, B, H, N, d]")
     P, B, H, N, d = o_parts.shape
-    if not (lse_parts.is_cuda and lse_parts.dtype == torch.float32 and lse_parts.is_contiguous()
-            and tuple(lse_parts.shape) == (P, B, H, N)):
-        raise TypeError("lse_parts must be a contiguous float32 CUDA tensor [P, B, H, N]")
+    _expect(lse_parts, "lse_parts", torch.float32, (P, B, H, N), o_parts.device, dense=True)
     if out is None:
         o = torch.empty((B, H, N, d), dtype=torch.float32, device=o_parts.device)
         lse = torch.empty((B, H, N), dtype=torch.float32, device=o_parts.device)
     else:
         o, lse = out
+        _expect(o, "o", torch.float32, (B, H, N, d), o_parts.device, dense=True)
+        _expect(lse, "lse", torch.float32, (B, H, N), o_parts.device, dense=True)
     _check(library().vitattn_merge(o_parts.data_ptr(), lse_parts.data_ptr(), P, o.data_ptr(), lse.data_ptr(), B, H,
                                    N, d, _stream_ptr(o_parts)))
     return o, lse
 
 
-def _require_dense(*ts):
-    if not _dense(*ts):
-        raise TypeError("the backward stage entry points take dense [B, H, N, d] tensors; use bwd() for strided ones")
+def _stage_args(q, names_bf16, names_f32_rows, names_f32_out, lse, workspace, B, H, N, d):
+    """Checks for the dense stage entry points: bf16 operands and fp32 outputs
+    of shape [B, H, N, d], lse [B, H, N], all contiguous on q's device."""
+    torch = _torch()
+    dev = q.device
+    for t, n in names_bf16:
+        _expect(t, n, torch.bfloat16, (B, H, N, d), dev, dense=True)
+    for t, n in names_f32_rows + names_f32_out:
+        _expect(t, n, torch.float32, (B, H, N, d), dev, dense=True)
+    if lse is not None:
+        _expect(lse, "lse", torch.float32, (B, H, N), dev, dense=True)
+    _expect_workspace(workspace, dev)
+
+
+def _shape4(t, name):
+    torch = _torch()
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dim() == 4):
+        raise TypeError(f"{name} must be a 4-D CUDA tensor [B, H, N, d]")
+    return tuple(int(n) for n in t.shape)
 
 
 def bwd_rowdot(o, dout, lse, workspace):
-    _require_dense(o, dout, lse)
-    B, H, N, d = dout.shape
+    B, H, N, d = _shape4(dout, "dout")
+    _stage_args(dout, [(dout, "dout")], [(o, "o")], [], lse, workspace, B, H, N, d)
     _check(library().vitattn_bwd_rowdot(o.data_ptr(), dout.data_ptr(), lse.data_ptr(), B, H, N, d, workspace.data_ptr(),
                                         workspace.numel() * workspace.element_size(), _stream_ptr(dout)))
 
 
 def bwd_dkdv(q, k, v, dout, lse, dk, dv, workspace, scale=None):
-    _require_dense(q, k, v, dout, lse, dk, dv)
-    B, H, N, d = q.shape
+    B, H, N, d = _shape4(q, "q")
+    _stage_args(q, [(q, "q"), (k, "k"), (v, "v"), (dout, "dout")], [], [(dk, "dk"), (dv, "dv")], lse, workspace,
+                B, H, N, d)
     _check(library().vitattn_bwd_dkdv(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
                                       dk.data_ptr(), dv.data_ptr(), B, H, N, d, _default_scale(d, scale),
                                       workspace.data_ptr(), workspace.numel() * workspace.element_size(),
@@ -259,8 +311,9 @@ def bwd_dkdv(q, k, v, dout, lse, dk, dv, workspace, scale=None):
 
 def bwd_dkdv_ds(q, k, v, dout, lse, dk, dv, workspace, scale=None):
     """The dK/dV stage of the dS mode (also writes the dS blocks into workspace)."""
-    _require_dense(q, k, v, dout, lse, dk, dv)
-    B, H, N, d = q.shape
+    B, H, N, d = _shape4(q, "q")
+    _stage_args(q, [(q, "q"), (k, "k"), (v, "v"), (dout, "dout")], [], [(dk, "dk"), (dv, "dv")], lse, workspace,
+                B, H, N, d)
     _check(library().vitattn_bwd_dkdv_ds(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
                                          dk.data_ptr(), dv.data_ptr(), B, H, N, d, _default_scale(d, scale),
                                          workspace.data_ptr(), workspace.numel() * workspace.element_size(),
@@ -269,16 +322,16 @@ def bwd_dkdv_ds(q, k, v, dout, lse, dk, dv, workspace, scale=None):
 
 def bwd_dq_from_ds(k, dq, workspace, scale=None):
     """The dQ stage of the dS mode, from the dS blocks bwd_dkdv_ds stored."""
-    _require_dense(k, dq)
-    B, H, N, d = k.shape
+    B, H, N, d = _shape4(k, "k")
+    _stage_args(k, [(k, "k")], [], [(dq, "dq")], None, workspace, B, H, N, d)
     _check(library().vitattn_bwd_dq_from_ds(k.data_ptr(), dq.data_ptr(), B, H, N, d, _default_scale(d, scale),
                                             workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                             _stream_ptr(k)))
 
 
 def bwd_dq(q, k, v, dout, lse, dq, workspace, scale=None):
-    _require_dense(q, k, v, dout, lse, dq)
-    B, H, N, d = q.shape
+    B, H, N, d = _shape4(q, "q")
+    _stage_args(q, [(q, "q"), (k, "k"), (v, "v"), (dout, "dout")], [], [(dq, "dq")], lse, workspace, B, H, N, d)
     _check(library().vitattn_bwd_dq(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), lse.data_ptr(),
                                     dq.data_ptr(), B, H, N, d, _default_scale(d, scale), workspace.data_ptr(),
                                     workspace.numel() * workspace.element_size(), _stream_ptr(q)))
@@ -306,8 +359,9 @@ def _dst(out, shape, like):
     torch = _torch()
     if out is None:
         return torch.empty(shape, dtype=like.dtype, device=like.device)
-    if not (out.is_cuda and out.dtype == like.dtype and out.is_contiguous() and tuple(out.shape) == tuple(shape)):
-        raise TypeError(f"out must be a contiguous {like.dtype} CUDA tensor of shape {tuple(shape)}")
+    if not (isinstance(out, torch.Tensor) and out.is_cuda and out.device == like.device and out.dtype == like.dtype
+            and out.is_contiguous() and tuple(out.shape) == tuple(shape)):
+        raise TypeError(f"out must be a contiguous {like.dtype} CUDA tensor of shape {tuple(shape)} on {like.device}")
     return out
 
 
@@ -349,8 +403,9 @@ def ulysses_unpack_out(recv, out=None):
 
 def _agg_shapes(q, k, v):
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        if not (t.is_cuda and t.dtype == _torch().bfloat16 and t.is_contiguous()):
-            raise TypeError(f"{n} must be a contiguous bfloat16 CUDA tensor")
+        if not (isinstance(t, _torch().Tensor) and t.is_cuda and t.dtype == _torch().bfloat16 and t.is_contiguous()
+                and t.device == k.device):
+            raise TypeError(f"{n} must be a contiguous bfloat16 CUDA tensor on the device of k")
     if q.dim() != 2 or k.dim() != 4 or k.shape != v.shape or k.shape[1] != q.shape[0] or k.shape[3] != q.shape[1]:
         raise ValueError("q must be [H, d] and k, v [M, H, C, d]")
     M, H, C, d = k.shape
@@ -374,9 +429,9 @@ def agg_bwd(q, k, v, o, lse, dout, scale=None):
     patches), dk and dv (fp32 [M,H,C,d])."""
     torch = _torch()
     M, H, C, d = _agg_shapes(q, k, v)
-    if not (dout.is_cuda and dout.dtype == torch.bfloat16 and dout.is_contiguous()
-            and tuple(dout.shape) == (M, H, d)):
-        raise TypeError("dout must be a contiguous bfloat16 CUDA tensor [M, H, d]")
+    _expect(dout, "dout", torch.bfloat16, (M, H, d), k.device, dense=True)
+    _expect(o, "o", torch.float32, (M, H, d), k.device, dense=True)
+    _expect(lse, "lse", torch.float32, (M, H), k.device, dense=True)
     lib = library()
     wsb = int(lib.vitattn_agg_bwd_workspace_bytes(M, H, C, d))
     ws = torch.empty(max(wsb, 4) // 4, dtype=torch.float32, device=k.device)
