@@ -53,18 +53,19 @@ def parse():
                         "zero operands, with the clock and power it runs at")
     p.add_argument("--no-compare", action="store_true",
                    help="skip timing the other backward mode after the timed region (for profiler runs)")
-    p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg", "d72", "d160", "bnhd"],
+    p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg", "d64", "d72", "d160", "bnhd"],
                    default="attention",
                    help="which workload to time (default: the attention forward+backward hot path at "
-                        "N=188,416, d=128; d72 / d160: the paper's other head dims; bnhd: the default "
-                        "workload with sequence-major operands)")
+                        "N=188,416, d=128; d64: the paper's own 188K shard, ViT-Base heads at d=64, B=4, "
+                        "same flops; d72 / d160: the paper's other head dims; bnhd: the default workload "
+                        "with sequence-major operands)")
     return p.parse_args()
 
 
 COPY_BYTES = 512 * 1024 * 1024
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_N188416_d128.json")
 ROW_TRAFFIC = {r: os.path.join(ROOT, "profiles", f"hbm_traffic_{r}.json")
-               for r in ("merge", "ulysses", "agg", "d72", "d160", "bnhd")}
+               for r in ("merge", "ulysses", "agg", "d64", "d72", "d160", "bnhd")}
 
 
 KERNEL_FILES = {
@@ -72,6 +73,7 @@ KERNEL_FILES = {
     "merge": ("vitattn_merge.hip",),
     "ulysses": ("vitattn_ulysses.hip",),
     "agg": ("vitattn_agg.hip",),
+    "d64": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
     "d72": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
     "d160": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
     "bnhd": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
@@ -452,6 +454,8 @@ def bench_row(args):
 # Sec. V-C, d = 160) as one GPU's Ulysses shard, and the headline workload
 # with every operand in the sequence-major layout an all-to-all produces.
 ATT_ROWS = {
+    "d64": dict(B=4, H=1, N=188416, d=64, bnhd=False,
+                doc="ViT-Base heads (d=64), the per-GPU shard of the paper's 188K run: B=4, H=1, N=188,416"),
     "d72": dict(B=1, H=2, N=65536, d=72, bnhd=False,
                 doc="ViT-10B heads (d=72; 64 heads, 2 per GPU at 32 Ulysses ranks), B=1, N=65,536"),
     "d160": dict(B=1, H=1, N=65536, d=160, bnhd=False,
