@@ -37,7 +37,8 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--config", type=int, default=4, help="workload id (4 = B1 H2 N188416 d128)")
+    p.add_argument("--workload", type=int, default=4,
+                   help="attention workload id of workloads.WORKLOADS (4 = B1 H2 N188416 d128, the metric's)")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
@@ -593,7 +594,7 @@ def main():
     import workloads
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    w = workloads.CONFIGS[args.config]
+    w = workloads.WORKLOADS[args.workload]
     B, H, N, d = w.shape
     x = workloads.make_inputs(w, with_dout=True)
     dev = torch.device("cuda:0")

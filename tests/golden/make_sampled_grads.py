@@ -8,7 +8,7 @@ sampled_grads_c<id>.npz next to itself, together with content hashes of the
 seeded inputs so a reader can detect generator drift.
 
 Only the oracle and the seeded input generator are called.
-Usage: python tests/golden/make_sampled_grads.py [config ids...]  (default 3 4)
+Usage: python tests/golden/make_sampled_grads.py [workload ids...]  (default 3 4)
 """
 import os
 import sys
@@ -33,21 +33,21 @@ _inputs = {}
 
 def _task(args):
     cid, b, h, keys = args
-    w = workloads.CONFIGS[cid]
+    w = workloads.WORKLOADS[cid]
     x = _inputs[cid]
     t0 = time.time()
     lse, D = oracle.row_statistics(x["q"], x["k"], x["v"], x["dout"], w.scale, b, h)
     dk, dv = oracle.key_rows(x["q"], x["k"], x["v"], x["dout"], w.scale, b, h, keys, lse, D)
-    print(f"config {cid} head ({b},{h}): {len(keys)} key rows in {time.time() - t0:.0f}s", flush=True)
+    print(f"{w.name} head ({b},{h}): {len(keys)} key rows in {time.time() - t0:.0f}s", flush=True)
     return cid, b, h, keys, dk, dv
 
 
 def main(cids):
     for cid in cids:
-        _inputs[cid] = workloads.make_inputs(workloads.CONFIGS[cid])
+        _inputs[cid] = workloads.make_inputs(workloads.WORKLOADS[cid])
     tasks = []
     for cid in cids:
-        rows = workloads.sampled_key_rows(workloads.CONFIGS[cid])
+        rows = workloads.sampled_key_rows(workloads.WORKLOADS[cid])
         for b, h in sorted({(int(r[0]), int(r[1])) for r in rows}):
             sel = (rows[:, 0] == b) & (rows[:, 1] == h)
             tasks.append((cid, b, h, rows[sel, 2]))
@@ -55,7 +55,7 @@ def main(cids):
     with mp.get_context("fork").Pool(procs) as pool:
         results = pool.map(_task, tasks, chunksize=1)
     for cid in cids:
-        w = workloads.CONFIGS[cid]
+        w = workloads.WORKLOADS[cid]
         rows = workloads.sampled_key_rows(w)
         dk = np.full((len(rows), w.d), np.nan)
         dv = np.full((len(rows), w.d), np.nan)

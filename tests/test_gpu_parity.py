@@ -40,12 +40,12 @@ def test_small_shapes_full_compare(B, H, N, d):
     assert_close(got, ref, label=f"small {B},{H},{N},{d}")
 
 
-def test_config1_full():
-    w = workloads.CONFIGS[1]
+def test_single_head_N1024_full():
+    w = workloads.WORKLOADS[1]
     x = workloads.make_inputs(w)
     got = hip64(run_hip(x, w.scale, backward=False))
     o, lse = oracle.forward(x["q"], x["k"], x["v"], w.scale)
-    assert_close(got, {"o": o, "lse": lse}, names=("o", "lse"), label="config 1")
+    assert_close(got, {"o": o, "lse": lse}, names=("o", "lse"), label=w.name)
 
 
 def _sampled_query_check(w, x, res, with_grad):
@@ -57,7 +57,7 @@ def _sampled_query_check(w, x, res, with_grad):
     if with_grad:
         got["dq"] = np64(res["dq"][sel])
         names = ("o", "lse", "dq")
-    return assert_close(got, ref, names=names, label=f"config {w.cid} sampled query rows")
+    return assert_close(got, ref, names=names, label=f"{w.name} sampled query rows")
 
 
 def _identities(w, x, res):
@@ -72,38 +72,39 @@ def _identities(w, x, res):
     r4 = ((f["v"] * g["dv"]).sum(ax) - (g["o"] * f["dout"]).sum(ax)).abs() / (
         f["v"].square().sum(ax) * g["dv"].square().sum(ax)).sqrt()
     rep = {"sum_dk": r1, "sum_dv": r2, "qdq_kdk": r3.max().item(), "vdv_odo": r4.max().item()}
-    print(f"config {w.cid} identities", rep, flush=True)
+    print(f"{w.name} identities", rep, flush=True)
     del f, g
     t.cuda.empty_cache()
     # Sum identities: each dS_ij is rounded to bf16 (relative 2^-9) and D comes
     # from the fp32 O, so sum_j dS_ij = 0 holds to about 1e-3 of |dS|; a wrong
     # term would leave an O(1) residual. The inner-product identities use the
-    # same dS on both sides and hold to fp32 rounding (calibrated on config 2:
+    # same dS on both sides and hold to fp32 rounding (calibrated on the 16,384-token workload:
     # 2.7e-3, 1.9e-3, 2.7e-9, 4.7e-6).
     assert rep["sum_dk"] < 1e-2 and rep["sum_dv"] < 1e-2, rep
     assert rep["qdq_kdk"] < 1e-4 and rep["vdv_odo"] < 1e-4, rep
 
 
-def test_config2_full_heads_sampled_rows_and_identities():
-    w = workloads.CONFIGS[2]
+def test_vit_block_N16384_x8_head_full_heads_sampled_rows_and_identities():
+    w = workloads.WORKLOADS[2]
     x = workloads.make_inputs(w)
     res = run_hip(x, w.scale)
     heads = [(0, 0), (1, 7)]  # the x8 stress head and an ordinary one
     ref = oracle.forward_backward(x["q"], x["k"], x["v"], x["dout"], w.scale, heads=heads)
     for b, h in heads:
         got = {n: np64(t[b, h]) for n, t in res.items()}
-        assert_close(got, {n: a[b, h] for n, a in ref.items()}, label=f"config 2 head ({b},{h})")
+        assert_close(got, {n: a[b, h] for n, a in ref.items()}, label=f"{w.name} head ({b},{h})")
     _sampled_query_check(w, x, res, with_grad=True)
     _identities(w, x, res)
 
 
 @pytest.mark.parametrize("store_ds", [False, True], ids=["recompute", "stored-ds"])
-@pytest.mark.parametrize("cid", [3, 4])
-def test_long_sequence_configs_sampled(cid, store_ds):
-    """Configs 3 and 4 at full size in both backward modes (the benchmark times
-    config 4 with the dS mode when its workspace fits)."""
-    w = workloads.CONFIGS[cid]
-    print(f"config {cid} ({'stored-ds' if store_ds else 'recompute'} backward): generating inputs", flush=True)
+@pytest.mark.parametrize("cid", [3, 4], ids=["H4_N65536_d128", "H2_N188416_d128"])
+def test_long_sequence_workloads_sampled(cid, store_ds):
+    """The 65,536-token (H=4, d=128) and 188,416-token (H=2, d=128) workloads
+    at full size in both backward modes (the benchmark times the 188,416-token
+    one with the dS mode when its workspace fits)."""
+    w = workloads.WORKLOADS[cid]
+    print(f"{w.name} ({'stored-ds' if store_ds else 'recompute'} backward): generating inputs", flush=True)
     x = workloads.make_inputs(w)
     res = run_hip(x, w.scale, store_ds=store_ds)
     _sampled_query_check(w, x, res, with_grad=True)
@@ -115,12 +116,12 @@ def test_long_sequence_configs_sampled(cid, store_ds):
     sel = tuple(torch().from_numpy(rows[:, i]).cuda() for i in range(3))
     got = {"dk": np64(res["dk"][sel]), "dv": np64(res["dv"][sel])}
     assert_close(got, {"dk": gold["dk"].astype(np.float64), "dv": gold["dv"].astype(np.float64)},
-                 names=("dk", "dv"), label=f"config {cid} sampled key rows")
+                 names=("dk", "dv"), label=f"{w.name} sampled key rows")
     _identities(w, x, res)
 
 
-def test_config5_one_million_tokens_sampled():
-    w = workloads.CONFIGS[5]
+def test_one_million_tokens_sampled():
+    w = workloads.WORKLOADS[5]
     x = workloads.make_inputs(w)
     res = run_hip(x, w.scale, backward=False)
     _sampled_query_check(w, x, res, with_grad=False)

@@ -25,8 +25,8 @@ def test_bf16_widening_roundtrip():
     np.testing.assert_array_equal(workloads.float32_to_bf16_bits(workloads.bf16_bits_to_float32(bits)), bits)
 
 
-def test_configs_match_the_paper_token_counts():
-    c = workloads.CONFIGS
+def test_workloads_match_the_paper_token_counts():
+    c = workloads.WORKLOADS
     assert c[4].N == 92 * 2048 == 368 * 512
     assert c[5].N == 1024 * 1024
     assert [c[i].d for i in range(1, 6)] == [64, 64, 128, 128, 64]
@@ -48,7 +48,7 @@ def test_inputs_are_deterministic_and_stress_head_is_scaled():
 
 def test_sampled_rows_distinct_and_in_range():
     for cid in (3, 4, 5):
-        w = workloads.CONFIGS[cid]
+        w = workloads.WORKLOADS[cid]
         r = workloads.sampled_query_rows(w)
         assert r.shape == (256, 3)
         assert len({tuple(x) for x in r}) == 256

@@ -13,12 +13,12 @@ for H local heads. The token counts are patch grids: 32x32, 128x128, 256x256,
 
 The ERA5 activations the paper trains on are not available; dense attention's
 run time does not depend on the values, so i.i.d. normal data stands in for
-them. Config 2 scales head 0's Q and K by 8 so that its softmax rows are close
+them. The 16,384-token ViT-block workload (id 2) scales head 0's Q and K by 8 so that its softmax rows are close
 to one-hot (logit standard deviation about 64), which stresses the running
 max and the bf16 rounding of P.
 
 Recipe: numpy Generator(PCG64(seed)); draw Q, K, V, dO in that order, each
-standard_normal((B,H,N,d), float32); multiply by sigma (and by 8 for config 2's
+standard_normal((B,H,N,d), float32); multiply by sigma (and by 8 for the id-2 workload's
 head 0 in Q and K; both multipliers are powers of two, so exact); round to
 bfloat16 with round-to-nearest-even.
 """
@@ -61,7 +61,7 @@ class Workload:
         return {"fwd": fwd, "bwd": bwd, "total": fwd + bwd}
 
 
-CONFIGS = {
+WORKLOADS = {
     1: Workload(1, "single_head_fwd_N1024_d64", 1, 1, 1024, 64, False, 1.0, 1001, 1.0, "full", (32, 32)),
     2: Workload(2, "vit_block_fwdbwd_B2_H16_N16384_d64", 2, 16, 16384, 64, True, 1.0, 1002, 8.0, "full",
                 (128, 128)),
