@@ -55,7 +55,7 @@ extern "C" {
 enum vitattn_status {
   VITATTN_OK = 0,
   VITATTN_E_INVAL = 1,       /* null/misaligned pointer, B/H/N < 1, non-finite or non-positive scale, size overflow */
-  VITATTN_E_UNSUPPORTED = 2, /* head dim d not supported (see above; vitattn_merge: d in {64, 128}) */
+  VITATTN_E_UNSUPPORTED = 2, /* head dim d not supported (see above) */
   VITATTN_E_WORKSPACE = 3,   /* workspace missing or smaller than vitattn_bwd_workspace_bytes() */
   VITATTN_E_HIP = 4,         /* the HIP runtime reported an error when launching */
   VITATTN_E_INTERNAL = 5     /* unexpected internal failure */
@@ -241,6 +241,8 @@ int vitattn_bwd_dq_from_ds(const void* k, float* dq, int B, int H, int N, int d,
  *   o, lse   : fp32 [B][H][N][d] and [B][H][N], written; they must not alias
  *              the partials.
  *   n_parts  : 1 .. VITATTN_MERGE_MAX_PARTS, else VITATTN_E_INVAL.
+ *   d        : any head dim the attention takes (a multiple of 8 up to 160),
+ *              else VITATTN_E_UNSUPPORTED.
  * A NaN partial LSE makes the merged row NaN. Bound by HBM bandwidth.
  */
 int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, float* o, float* lse, int B, int H,

@@ -265,9 +265,7 @@ int vitattn_bwd_strided(const void* q, vitattn_strides sq, const void* k, vitatt
 int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, float* o, float* lse, int B, int H,
                   int N, int d, void* stream) {
   try {
-    if (B < 1 || H < 1 || N < 1) return VITATTN_E_INVAL;
-    if (d != 64 && d != 128) return VITATTN_E_UNSUPPORTED;
-    int st = check_rows(B, H, N, d);
+    int st = check_sizes(B, H, N, d);  // d: a multiple of 8 up to 160, as for the attention
     if (st != VITATTN_OK) return st;
     if (n_parts < 1 || n_parts > VITATTN_MERGE_MAX_PARTS) return VITATTN_E_INVAL;
     if (!aligned16(o_parts) || !aligned16(lse_parts) || !aligned16(o) || !aligned16(lse)) return VITATTN_E_INVAL;

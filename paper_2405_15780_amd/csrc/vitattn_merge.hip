@@ -5,8 +5,11 @@
 //     LSE_i = log sum_s exp(LSE_s,i),   O_i = sum_s exp(LSE_s,i - LSE_i) O_s,i
 //
 // computed here with the largest partial LSE subtracted first. Bound by HBM:
-// each row reads P (d + 1) floats and writes d + 1. One thread per four
-// columns of a row; a block covers 256 / (d / 4) rows.
+// each row reads P (d + 1) floats and writes d + 1. Thread t of the grid
+// takes float4 t of the output (row t / (d/4), its d/4 float4 pieces in
+// order), so a wave moves consecutive 16-byte pieces across row boundaries;
+// the row width is a template parameter (TPR = d/4 pieces, d a multiple of 8
+// up to 160), which keeps the division by it a multiply.
 #include <math.h>
 
 #include "vitattn_common.h"
@@ -14,14 +17,13 @@
 
 namespace vitattn {
 
-template <int D>
+template <int TPR>
 __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict__ o_parts,
                                                          const float* __restrict__ lse_parts, float* __restrict__ o,
                                                          float* __restrict__ lse, int P, long rows) {
-  constexpr int TPR = D / 4;        // threads per row
-  constexpr int RPB = 256 / TPR;    // rows per block
-  const long row = (long)blockIdx.x * RPB + threadIdx.x / TPR;
-  const int c4 = threadIdx.x % TPR;
+  const long t = (long)blockIdx.x * 256 + threadIdx.x;
+  const long row = t / TPR;
+  const int c4 = (int)(t - row * TPR);
   if (row >= rows) return;
   // fmaxf ignores a NaN partial here; its weight below is NaN and poisons the row
   float m = -INFINITY;
@@ -31,7 +33,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
   for (int p = 0; p < P; ++p) {
     const size_t pr = (size_t)p * rows + row;
     const float w = expf(lse_parts[pr] - m);
-    const float4 x = reinterpret_cast<const float4*>(o_parts + pr * D)[c4];
+    const float4 x = reinterpret_cast<const float4*>(o_parts + pr * (4 * TPR))[c4];
     tot += w;
     acc.x += w * x.x;
     acc.y += w * x.y;
@@ -39,24 +41,30 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
     acc.w += w * x.w;
   }
   const float inv = 1.f / tot;
-  reinterpret_cast<float4*>(o + (size_t)row * D)[c4] = make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+  reinterpret_cast<float4*>(o + (size_t)row * (4 * TPR))[c4] =
+      make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
   if (c4 == 0) lse[row] = m + logf(tot);
 }
 
-template __global__ void attn_merge_kernel<128>(const float* __restrict__, const float* __restrict__,
-                                                float* __restrict__, float* __restrict__, int, long);
-template __global__ void attn_merge_kernel<64>(const float* __restrict__, const float* __restrict__,
-                                               float* __restrict__, float* __restrict__, int, long);
-
-template <int D>
-static hipError_t merge_d(const MergeArgs& a) {
-  constexpr int RPB = 256 / (D / 4);
+template <int TPR>
+static hipError_t merge_t(const MergeArgs& a) {
   const long rows = (long)a.BH * a.N;
-  hipLaunchKernelGGL(attn_merge_kernel<D>, dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), 0, a.stream,
-                     a.o_parts, a.lse_parts, a.o, a.lse, a.P, rows);
+  const long blocks = (rows * TPR + 255) / 256;
+  hipLaunchKernelGGL(attn_merge_kernel<TPR>, dim3((unsigned)blocks), dim3(256), 0, a.stream, a.o_parts, a.lse_parts,
+                     a.o, a.lse, a.P, rows);
   return hipGetLastError();
 }
 
-hipError_t launch_merge(const MergeArgs& a) { return a.d == 128 ? merge_d<128>(a) : merge_d<64>(a); }
+// d = 8 .. 160 in steps of 8: TPR = 2 .. 40 in steps of 2
+template <int TPR>
+static hipError_t merge_dispatch(const MergeArgs& a) {
+  if constexpr (TPR > 40) {
+    return hipErrorInvalidValue;
+  } else {
+    return a.d == 4 * TPR ? merge_t<TPR>(a) : merge_dispatch<TPR + 2>(a);
+  }
+}
+
+hipError_t launch_merge(const MergeArgs& a) { return merge_dispatch<2>(a); }
 
 }  // namespace vitattn

@@ -202,7 +202,8 @@ def test_bwd_kv_workspace_is_sized_by_query_rows():
 
 @pytest.mark.parametrize("kw,expected", [
     (dict(P=0), E_INVAL), (dict(P=-3), E_INVAL), (dict(P=65537), E_INVAL), (dict(N=0), E_INVAL),
-    (dict(d=96), E_UNSUP), (dict(override={0: None}), E_INVAL), (dict(override={3: 4104}), E_INVAL),
+    (dict(d=100), E_UNSUP), (dict(d=168), E_UNSUP), (dict(d=0), E_UNSUP), (dict(override={0: None}), E_INVAL),
+    (dict(override={3: 4104}), E_INVAL),
 ])
 def test_merge_rejects_bad_arguments(kw, expected):
     b = Bufs()

@@ -127,7 +127,7 @@ def test_dq_overwrite_ignores_previous_contents():
     assert rel_l2(np64(dv), dv_ref) <= 1e-2
 
 
-@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("d", [8, 64, 72, 128, 136, 160])
 def test_merge_kernel_against_oracle(d):
     import paper_2405_15780_amd as va
 
