@@ -652,7 +652,12 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
 // the transpose of the stored order; two ds_read_b64_tr_b16 per 16 keys build
 // it (lane j of a 16-lane group supplies the address of the 4 consecutive
 // queries of key 16 ks + 4 h + j/4, so result lane i gets query i's entry of
-// 4 consecutive keys).
+// 4 consecutive keys). In the stored order, the 16 chunks (16 bytes) that a
+// half-wave reads fall into only 4 of the 16 bank groups (chunk index mod 16),
+// a 4-way LDS bank conflict on every read; so the DMA permutes the block's
+// chunks, LDS slot s holding chunk s ^ (((s >> 5) & 3) << 2) (its own
+// inverse, within the block), which spreads each half-wave's chunks over all
+// 16 groups.
 template <int D, int NW, int RING>
 __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ ds, float* __restrict__ dq, const Map mk,
@@ -693,9 +698,18 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
   dma.init(wave, lane, ldk, chr);
   TrFrag<D> tf;
   tf.init(lane);
-  // dS^T operand reads: per-lane byte offset within the wave's 2 KB block
+  // dS^T operand reads: per-lane byte offsets within the wave's 2 KB block,
+  // through the chunk permutation (chunk c of the stored order sits in slot
+  // c ^ (m << 2), m = bits 5-6 of c; the second read of a pair, 8 chunks on,
+  // flips bit 3 of the slot, hence the XOR)
   const int g = lane >> 4, j = lane & 15;
-  const int soff = (g & 1) * 1024 + (j & 1) * 512 + (4 * (g >> 1) + (j >> 2)) * 16 + 8 * ((j >> 1) & 1);
+  const int c0 = (g & 1) * 64 + (j & 1) * 32 + 4 * (g >> 1) + (j >> 2);  // stored-order chunk
+  const int soff_lo = 16 * (c0 ^ (((j & 1) | ((g & 1) << 1)) << 2)) + 8 * ((j >> 1) & 1);
+  const int soff_hi = soff_lo ^ 128;
+  // DMA: lane L of request i fills slot 64 i + L with chunk (64 i + L) ^ (m << 2)
+  int ds_voff[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) ds_voff[i] = 16 * ((64 * i + lane) ^ ((((lane >> 5) & 1) | (i << 1)) << 2));
 
   // this head's dS rows start here; key block kb's row of nqb blocks follows
   const uint16_t* ds_head = ds + (size_t)bh * nkb * nqb * 1024;
@@ -708,7 +722,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
 #pragma unroll
     for (int i = 0; i < 2; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)(sdst + wave * 2048 + i * 1024), 16,
-                                               qblock * 2048 + i * 1024 + lane * 16, 0, 0, 0);
+                                               qblock * 2048 + ds_voff[i], 0, 0, 0);
   };
   // vector loads per wave per tile: its K share (none for the waves left
   // without one when a K tile is fewer instructions than waves) and 2 for dS
@@ -741,9 +755,8 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
     bf16x8 dsb[2];
 #pragma unroll
     for (int kh = 0; kh < 2; ++kh) {
-      const char* p0 = sb + soff + kh * 256;
-      bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
-      bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0 + 128));
+      bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(sb + soff_lo + kh * 256));
+      bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(sb + soff_hi + kh * 256));
       dsb[kh][0] = lo[0]; dsb[kh][1] = lo[1]; dsb[kh][2] = lo[2]; dsb[kh][3] = lo[3];
       dsb[kh][4] = hi[0]; dsb[kh][5] = hi[1]; dsb[kh][6] = hi[2]; dsb[kh][7] = hi[3];
     }
