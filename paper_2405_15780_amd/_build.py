@@ -17,7 +17,7 @@ HIP_FLAGS = [
     "-std=c++17",
     "-fPIC",
     "-shared",
-    "-Wall",
+    "-Wall", "-Wextra",
     # packed fp32 VALU forms stay disabled on this target
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # keep matrix-core accumulators in VGPR form: otherwise the allocator

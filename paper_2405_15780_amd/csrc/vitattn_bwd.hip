@@ -555,7 +555,10 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
         if constexpr (i + 1 < NOPS) aq[(i + 1) & 1] = load_op(i + 1);
         if constexpr (i < NS) {
           if constexpr (i % KK == 0) nxt[i / KK] = zero16();
-          nxt[i / KK] = mfma32(aq[i & 1], i < KK ? qf[i] : gf[i - KK], nxt[i / KK]);
+          if constexpr (i < KK)
+            nxt[0] = mfma32(aq[i & 1], qf[i], nxt[0]);
+          else
+            nxt[1] = mfma32(aq[i & 1], gf[i - KK], nxt[1]);
         } else {
           constexpr int t = i - NS;
           dqacc[t % NCB] = mfma32(aq[i & 1], dsb[t / NCB], dqacc[t % NCB]);
