@@ -33,3 +33,4 @@ from .binding import (  # noqa: F401
     workspace_bytes,
     workspace_bytes_kv,
 )
+from .autograd import attention  # noqa: F401,E402
