@@ -30,7 +30,29 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(const float* __restrict
   for (int p = 0; p < P; ++p) m = fmaxf(m, lse_parts[(size_t)p * rows + row]);
   float tot = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int p = 0; p < P; ++p) {
+  // partials in groups of four: the group's loads are issued before any is used
+  constexpr int G = 4;
+  int p0 = 0;
+  for (; p0 + G <= P; p0 += G) {
+    float4 x[G];
+    float w[G];
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const size_t pr = (size_t)(p0 + u) * rows + row;
+      x[u] = reinterpret_cast<const float4*>(o_parts + pr * (4 * TPR))[c4];
+      w[u] = lse_parts[pr];
+    }
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const float wu = expf(w[u] - m);
+      tot += wu;
+      acc.x += wu * x[u].x;
+      acc.y += wu * x[u].y;
+      acc.z += wu * x[u].z;
+      acc.w += wu * x[u].w;
+    }
+  }
+  for (int p = p0; p < P; ++p) {
     const size_t pr = (size_t)p * rows + row;
     const float w = expf(lse_parts[pr] - m);
     const float4 x = reinterpret_cast<const float4*>(o_parts + pr * (4 * TPR))[c4];
