@@ -54,11 +54,11 @@ def parse():
                         "zero operands, with the clock and power it runs at")
     p.add_argument("--no-compare", action="store_true",
                    help="skip timing the other backward mode after the timed region (for profiler runs)")
-    p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg", "d64", "d72", "d160", "bnhd"],
+    p.add_argument("--row", choices=["attention", "merge", "ulysses", "agg", "d64", "m1", "d72", "d160", "bnhd"],
                    default="attention",
                    help="which workload to time (default: the attention forward+backward hot path at "
                         "N=188,416, d=128; d64: the paper's own 188K shard, ViT-Base heads at d=64, B=4, "
-                        "same flops; d72 / d160: the paper's other head dims; bnhd: the default workload "
+                        "same flops; m1: ViT-Base at 1M tokens, one head; d72 / d160: the paper's other head dims; bnhd: the default workload "
                         "with sequence-major operands)")
     return p.parse_args()
 
@@ -66,7 +66,7 @@ def parse():
 COPY_BYTES = 512 * 1024 * 1024
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_N188416_d128.json")
 ROW_TRAFFIC = {r: os.path.join(ROOT, "profiles", f"hbm_traffic_{r}.json")
-               for r in ("merge", "ulysses", "agg", "d64", "d72", "d160", "bnhd")}
+               for r in ("merge", "ulysses", "agg", "d64", "m1", "d72", "d160", "bnhd")}
 
 
 KERNEL_FILES = {
@@ -75,6 +75,7 @@ KERNEL_FILES = {
     "ulysses": ("vitattn_ulysses.hip",),
     "agg": ("vitattn_agg.hip",),
     "d64": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
+    "m1": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
     "d72": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
     "d160": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
     "bnhd": ("vitattn_fwd.hip", "vitattn_bwd.hip"),
@@ -457,6 +458,8 @@ def bench_row(args):
 ATT_ROWS = {
     "d64": dict(B=4, H=1, N=188416, d=64, bnhd=False,
                 doc="ViT-Base heads (d=64), the per-GPU shard of the paper's 188K run: B=4, H=1, N=188,416"),
+    "m1": dict(B=1, H=1, N=1048576, d=64, bnhd=False,
+               doc="ViT-Base heads at 1M tokens (d=64; 1 head per GPU at 16 Ulysses ranks), B=1, H=1, N=1,048,576"),
     "d72": dict(B=1, H=2, N=65536, d=72, bnhd=False,
                 doc="ViT-10B heads (d=72; 64 heads, 2 per GPU at 32 Ulysses ranks), B=1, N=65,536"),
     "d160": dict(B=1, H=1, N=65536, d=160, bnhd=False,
