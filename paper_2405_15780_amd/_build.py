@@ -33,16 +33,38 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: cannot build the gfx950 attention library")
 
 
-def build(verbose: bool = False) -> str:
-    """Always recompiles; writes LIB_PATH atomically and returns it."""
-    tmp = LIB_PATH + f".tmp{os.getpid()}"
-    cmd = [hipcc(), *HIP_FLAGS, "-o", tmp, *[os.path.join(CSRC, s) for s in SOURCES]]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB_PATH)
+# Debug variant for the tests: every kernel first fills its LDS with NaN bytes,
+# so a read of LDS that nothing wrote shows up as NaN (never used by the
+# package itself; tests load it explicitly).
+LDS_POISON_LIB_PATH = os.path.join(HERE, "libvitattn_ldspoison.so")
+
+
+def _command(out: str, extra=()) -> list:
+    return [hipcc(), *HIP_FLAGS, *extra, "-o", out, *[os.path.join(CSRC, s) for s in SOURCES]]
+
+
+def build(verbose: bool = False, lds_poison: bool = True) -> str:
+    """Always recompiles; writes LIB_PATH (and, with lds_poison, the LDS-poison
+    debug variant, compiled alongside) atomically and returns LIB_PATH."""
+    jobs = [(LIB_PATH, ())]
+    if lds_poison:
+        jobs.append((LDS_POISON_LIB_PATH, ("-DVITATTN_DEBUG_LDS_POISON",)))
+    procs = []
+    for path, extra in jobs:
+        tmp = path + f".tmp{os.getpid()}"
+        cmd = _command(tmp, extra)
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((path, tmp, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))
+    failed = []
+    for path, tmp, p in procs:
+        out, err = p.communicate()
+        if p.returncode != 0:
+            failed.append(f"{os.path.basename(path)}: hipcc failed ({p.returncode}):\n{out}\n{err}")
+        else:
+            os.replace(tmp, path)
+    if failed:
+        raise RuntimeError("\n".join(failed))
     return LIB_PATH
 
 

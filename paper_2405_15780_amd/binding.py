@@ -61,6 +61,17 @@ class VitattnError(RuntimeError):
         super().__init__(status_str(status))
 
 
+def open_library(path):
+    """ctypes handle of a built library at `path` with every entry point's
+    signature set (library() uses it for the package's own build)."""
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
 def library():
     """Load libvitattn.so once. Raises if it has not been built."""
     global _lib
@@ -68,12 +79,7 @@ def library():
         if _lib is None:
             if not os.path.exists(LIB_PATH):
                 raise ImportError(f"{LIB_PATH} is missing: build it with paper_2405_15780_amd._build.build()")
-            lib = ctypes.CDLL(LIB_PATH)
-            for name, (res, args) in _SIGNATURES.items():
-                fn = getattr(lib, name)
-                fn.restype = res
-                fn.argtypes = args
-            _lib = lib
+            _lib = open_library(LIB_PATH)
     return _lib
 
 

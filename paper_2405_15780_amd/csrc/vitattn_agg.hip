@@ -179,6 +179,7 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
     float scale) {
   constexpr int LPR = D / 8, RPC = 64 / LPR, G = kAggChunkGroup;
   __shared__ __attribute__((aligned(16))) float red[4][D];
+  debug_poison_lds(red);
   const int h = blockIdx.x % H, mb = blockIdx.x / H;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = lane / LPR, cg = lane % LPR;
@@ -256,6 +257,7 @@ __global__ __launch_bounds__(256) void attn_agg_bwd_kernel(
 __global__ __launch_bounds__(1024) void attn_agg_dq_kernel(const float* __restrict__ partial, float* __restrict__ dq,
                                                            int groups, int HD, float scale) {
   __shared__ float red[64][17];
+  debug_poison_lds(red);
   const int col = threadIdx.x & 15, r = threadIdx.x >> 4;
   const int t = blockIdx.x * 16 + col;
   float s = 0.f;

@@ -139,6 +139,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // widest tile needs the two-slot form to fit in LDS.
   constexpr int XR = D == 160 ? 2 : RING;
   __shared__ __attribute__((aligned(16))) uint4 xbuf[XR][kBwdWaves][2][2][64];
+  debug_poison_lds(qbuf0, qbuf1, qbuf2, gbuf0, gbuf1, gbuf2, sbuf0, sbuf1, sbuf2, xbuf);
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_ktiles;
@@ -455,6 +456,7 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
   static_assert(RING == 6, "one variable per slot");
   char* const kbuf[RING] = {kbuf0, kbuf1, kbuf2, kbuf3, kbuf4, kbuf5};
   char* const vbuf[RING] = {vbuf0, vbuf1, vbuf2, vbuf3, vbuf4, vbuf5};
+  debug_poison_lds(kbuf0, kbuf1, kbuf2, kbuf3, kbuf4, kbuf5, vbuf0, vbuf1, vbuf2, vbuf3, vbuf4, vbuf5);
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;
@@ -686,6 +688,10 @@ __global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_ds_kernel(
   // (a ring of four leaves the last two slot pairs unreferenced, and unallocated)
   char* const kbuf[6] = {kbuf0, kbuf1, kbuf2, kbuf3, RING > 4 ? kbuf4 : kbuf0, RING > 4 ? kbuf5 : kbuf1};
   char* const sbuf[6] = {sbuf0, sbuf1, sbuf2, sbuf3, RING > 4 ? sbuf4 : sbuf0, RING > 4 ? sbuf5 : sbuf1};
+  if constexpr (RING > 4)
+    debug_poison_lds(kbuf0, kbuf1, kbuf2, kbuf3, kbuf4, kbuf5, sbuf0, sbuf1, sbuf2, sbuf3, sbuf4, sbuf5);
+  else
+    debug_poison_lds(kbuf0, kbuf1, kbuf2, kbuf3, sbuf0, sbuf1, sbuf2, sbuf3);
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;

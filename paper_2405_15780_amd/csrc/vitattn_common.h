@@ -254,6 +254,24 @@ struct TileDma {
   }
 };
 
+// Debug builds only (-DVITATTN_DEBUG_LDS_POISON): a kernel first fills its
+// LDS buffers with all-ones bytes (NaN as bf16 and as fp32), so that any read
+// of LDS that nothing wrote turns its outputs into NaN. Without the define
+// this emits no code and no barrier.
+template <typename... A>
+__device__ __forceinline__ void debug_poison_lds(A&... bufs) {
+#ifdef VITATTN_DEBUG_LDS_POISON
+  auto fill = [](void* p, unsigned bytes) {
+    uint32_t* w = static_cast<uint32_t*>(p);
+    for (unsigned i = threadIdx.x; i < bytes / 4; i += blockDim.x) w[i] = 0xffffffffu;
+  };
+  (fill(static_cast<void*>(&bufs), (unsigned)sizeof(bufs)), ...);
+  __syncthreads();
+#else
+  ((void)bufs, ...);
+#endif
+}
+
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 // Wait until at most CNT of this wave's vector memory loads are in flight
 // (loads complete in issue order for this count).

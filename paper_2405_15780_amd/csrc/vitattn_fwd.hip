@@ -85,6 +85,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   __shared__ __attribute__((aligned(1024))) char vbuf1[TILE_BYTES];
   char* const kbuf[2] = {kbuf0, kbuf1};
   char* const vbuf[2] = {vbuf0, vbuf1};
+  debug_poison_lds(kbuf0, kbuf1, vbuf0, vbuf1);
 
   const int work = xcd_remap(blockIdx.x, total);
   const int bh = work / n_qtiles;
