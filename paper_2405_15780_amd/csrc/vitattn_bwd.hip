@@ -11,9 +11,12 @@
 //      registers); streams K and V in tiles of 64 keys:
 //        S^T = K Q^T, P^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T
 // Splitting dQ from dK/dV costs one extra recomputation of S and dP but needs
-// no atomics, so results are deterministic. As in the forward pass, operands
+// no atomics for dQ. The only atomics are those of the dK/dV kernel's split
+// key blocks (two fp32 adds onto zero per element, which commute exactly), so
+// results are deterministic. As in the forward pass, operands
 // may have any batch / head / row strides, and a head dim d below the tile
 // width D is padded with zero columns on load and cut off on store.
+#include <atomic>
 #include <type_traits>
 
 #include "vitattn_common.h"
@@ -103,13 +106,19 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 // that tile's DMA requests: loads and stores share one completion counter
 // and may complete out of order with respect to each other, so a store must
 // never sit between a DMA request and the wait for it.
+//
+// Grid balance: with one workgroup per CU, a grid that is not a whole number
+// of rounds leaves CUs idle in its last round. Workgroups below n_whole each
+// own a key block and every query; the key blocks after them (at most half a
+// round of them) are split into two workgroups each, one per half of the
+// query tiles, which add their dK and dV into rows the launch zeroed first.
 template <int D, bool STORE_DS>
 __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
     float* __restrict__ dk, float* __restrict__ dv, uint16_t* __restrict__ ds_out, const Map mq, const Map mk,
-    const Map mv, const Map mg, const Map mdk, const Map mdv, int H, int dr, int Nq, int Nk, int n_ktiles, int total,
-    float c, float scale) {
+    const Map mv, const Map mg, const Map mdk, const Map mdv, int H, int dr, int Nq, int Nk, int n_ktiles,
+    int n_whole, float c, float scale) {
   constexpr int KK = D / 16, NCB = D / 32;
   constexpr int PH = KK;           // ops per phase
   constexpr int NOPS = 4 * PH;     // ops per tile
@@ -141,7 +150,20 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   __shared__ __attribute__((aligned(16))) uint4 xbuf[XR][kBwdWaves][2][2][64];
   debug_poison_lds(qbuf0, qbuf1, qbuf2, gbuf0, gbuf1, gbuf2, sbuf0, sbuf1, sbuf2, xbuf);
 
-  const int work = xcd_remap(blockIdx.x, total);
+  // this workgroup's key block (work item) and query tiles [t0, t1)
+  const int n_qt_real = (Nq + kDkvBQ - 1) / kDkvBQ;
+  const bool split = (int)blockIdx.x >= n_whole;
+  int work, t0 = 0, t1 = n_qt_real;
+  if (!split) {
+    work = xcd_remap(blockIdx.x, n_whole);
+  } else {
+    const int part = blockIdx.x - n_whole;
+    work = n_whole + (part >> 1);
+    if (part & 1) t0 = n_qt_real >> 1;
+    else t1 = n_qt_real >> 1;
+  }
+  // query rows at or past qend read as zeros (the ragged end, or the other half's rows)
+  const int qend = min(Nq, t1 * kDkvBQ);
   const int bh = work / n_ktiles;
   const int kt = work - bh * n_ktiles;
   const int tid = threadIdx.x;
@@ -152,10 +174,10 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // queries, dO and the row statistics have Nq rows per (b, h); K, V, dK, dV have Nk
   const int chr = dr >> 3;  // 16-byte chunks of a row that hold data
   const int ldq = 2 * mq.ld, ldg = 2 * mg.ld;  // row strides in bytes
-  const rsrc_t rq = make_rsrc(q + mq.head(bh, H), (unsigned)(Nq * ldq));
-  const rsrc_t rg = make_rsrc(dout + mg.head(bh, H), (unsigned)(Nq * ldg));
-  const rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)Nq * 4);
-  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)Nq * 4);
+  const rsrc_t rq = make_rsrc(q + mq.head(bh, H), (unsigned)(qend * ldq));
+  const rsrc_t rg = make_rsrc(dout + mg.head(bh, H), (unsigned)(qend * ldg));
+  const rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)qend * 4);
+  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)qend * 4);
 
   // held fragments (B operands, columns = this block's keys): K for role P, V for role dS
   const int key = kt * kDkvBK + kb * 32 + (lane & 31);
@@ -182,16 +204,17 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero16();
 
-  // STORE_DS: the dS operands of the wave's previous tile, not yet stored
-  const int n_qt_real = (Nq + kDkvBQ - 1) / kDkvBQ;
+  // Tiles are numbered from t0 in the loops below. STORE_DS: the dS operands
+  // of the wave's previous tile, not yet stored (padding tiles past t1 are not).
   bf16x8 pend[2][2];
   int pend_tile = -1;
   auto flush_ds = [&]() {
     if constexpr (STORE_DS) {
-      if (pend_tile >= 0 && pend_tile < n_qt_real) {
+      if (pend_tile >= 0 && pend_tile < t1 - t0) {
         // blocks (key block, query blocks 2t and 2t+1) of this head, 2 KB each
         const size_t nkb = (size_t)n_ktiles * kBwdWaves, nqb = 2 * (size_t)n_qt_real;
-        uint16_t* dst = ds_out + (((size_t)bh * nkb + (size_t)kt * kBwdWaves + kb) * nqb + 2 * pend_tile) * 1024;
+        uint16_t* dst =
+            ds_out + (((size_t)bh * nkb + (size_t)kt * kBwdWaves + kb) * nqb + 2 * (size_t)(t0 + pend_tile)) * 1024;
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
@@ -205,9 +228,10 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 
   auto issue_tile = [&](auto slot_tag, int t) {
     constexpr int SL = decltype(slot_tag)::value;
-    dma.issue(rq, t * kDkvBQ, ldq, qbuf[SL]);
-    dmg.issue(rg, t * kDkvBQ, ldg, gbuf[SL]);
-    stats_dma(rd, rl, t * kDkvBQ, sbuf[SL], lane);
+    const int row0 = (t0 + t) * kDkvBQ;
+    dma.issue(rq, row0, ldq, qbuf[SL]);
+    dmg.issue(rg, row0, ldg, gbuf[SL]);
+    stats_dma(rd, rl, row0, sbuf[SL], lane);
   };
 
   // One tile of one role, in ring slot SL. Role P: S/P/dV; role dS: dP/dS/dK.
@@ -320,7 +344,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // Iteration t: role P on tile t (slot t % 3), role dS on tile t-1, tile t+1
   // requested into slot (t+1) % 3. Rounding the tile count to 1 mod 3 lets
   // iterations 1 .. n_pad-1 run in groups of three with fixed slots.
-  const int n_qt = (Nq + kDkvBQ - 1) / kDkvBQ;
+  const int n_qt = t1 - t0;
   const int n_pad = n_qt + (3 + 1 - n_qt % 3) % 3;
   // Each role runs its own copy of the tile loop, so that the compiler sees
   // in the dS waves' copy that (with STORE_DS) they never have a DMA request
@@ -405,10 +429,34 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int col = 32 * cb + 8 * g + 4 * h;  // d is a multiple of 8: four columns are all in or all out
-        if (col < dr)
-          *reinterpret_cast<float4*>(out + col) =
-              make_float4(acc[cb][4 * g] * f, acc[cb][4 * g + 1] * f, acc[cb][4 * g + 2] * f, acc[cb][4 * g + 3] * f);
+        if (col < dr) {
+          if (split) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) unsafeAtomicAdd(out + col + e, acc[cb][4 * g + e] * f);
+          } else {
+            *reinterpret_cast<float4*>(out + col) = make_float4(acc[cb][4 * g] * f, acc[cb][4 * g + 1] * f,
+                                                                acc[cb][4 * g + 2] * f, acc[cb][4 * g + 3] * f);
+          }
+        }
       }
+  }
+}
+
+// Zeroes dK and dV over the key blocks of work items first .. first +
+// gridDim.x/2 - 1 (rows below Nk, columns below dr), which the dK/dV kernel's
+// split workgroups then add into.
+__global__ __launch_bounds__(256) void zero_key_blocks_kernel(float* __restrict__ dk, float* __restrict__ dv,
+                                                              const Map mdk, const Map mdv, int H, int dr, int Nk,
+                                                              int n_ktiles, int first) {
+  const int work = first + (blockIdx.x >> 1);
+  const bool is_v = blockIdx.x & 1;
+  const int bh = work / n_ktiles, kt = work - bh * n_ktiles;
+  const Map& m = is_v ? mdv : mdk;
+  float* base = (is_v ? dv : dk) + m.head(bh, H);
+  const int c4 = dr >> 2, key0 = kt * kDkvBK, rows = min(kDkvBK, Nk - key0);
+  for (int i = threadIdx.x; i < rows * c4; i += 256) {
+    const int r = i / c4, c = i - r * c4;
+    *reinterpret_cast<float4*>(base + (long long)(key0 + r) * m.ld + 4 * c) = make_float4(0.f, 0.f, 0.f, 0.f);
   }
 }
 
@@ -827,13 +875,44 @@ static hipError_t rowdot_l(const BwdArgs& a) {
   return hipGetLastError();
 }
 
+// Workgroups of the dK/dV kernel resident on the current device at once
+// (0 if the runtime cannot say), looked up once per device.
+template <int D, bool STORE_DS>
+static int dkdv_resident_workgroups() {
+  static std::atomic<int> known[64];  // per device ordinal; 0 = not looked up, -1 = unknown
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int n = known[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    int per_cu = 0, cus = 0;
+    n = -1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dkdv_kernel<D, STORE_DS>, 2 * kBwdThreads,
+                                                     0) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && per_cu * cus > 0)
+      n = per_cu * cus;
+    known[dev].store(n, std::memory_order_relaxed);
+  }
+  return n > 0 ? n : 0;
+}
+
 template <int D, bool STORE_DS>
 static hipError_t dkdv_s(const BwdArgs& a) {
   const int n_kt = (a.Nk + kDkvBK - 1) / kDkvBK;
   const int total = a.BH * n_kt;
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS>), dim3(total), dim3(2 * kBwdThreads), 0, a.stream, a.q,
+  // A last round at most half full is split in two halves of the query range
+  // (when there are two query tiles to split), so that it takes half as long.
+  const int slots = dkdv_resident_workgroups<D, STORE_DS>();
+  const int tail = slots > 0 ? total % slots : 0;
+  int n_whole = total;
+  if (tail > 0 && 2 * tail <= slots && (a.Nq + kDkvBQ - 1) / kDkvBQ >= 2) {
+    n_whole = total - tail;
+    hipLaunchKernelGGL(zero_key_blocks_kernel, dim3(2 * tail), dim3(256), 0, a.stream, a.dk, a.dv, a.mdk, a.mdv, a.H,
+                       a.d, a.Nk, n_kt, n_whole);
+  }
+  const int grid = n_whole + 2 * (total - n_whole);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS>), dim3(grid), dim3(2 * kBwdThreads), 0, a.stream, a.q,
                      a.k, a.v, a.dout, a.drow, a.lse2, a.dk, a.dv, a.ds, a.mq, a.mk, a.mv, a.mg, a.mdk, a.mdv, a.H,
-                     a.d, a.Nq, a.Nk, n_kt, total, a.scale * kLog2e, a.scale);
+                     a.d, a.Nq, a.Nk, n_kt, n_whole, a.scale * kLog2e, a.scale);
   return hipGetLastError();
 }
 template <int D>

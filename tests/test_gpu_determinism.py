@@ -1,8 +1,10 @@
 """Run-to-run bitwise determinism of every entry point that has no fixed
 summation order elsewhere: the dS-mode backward (dK/dV kernel with its dS
 stores, dQ from the stored blocks), dQ accumulated over key segments, the
-merge, and the channel aggregation with its dq partials. None uses atomics,
-so two runs on the same inputs must agree bit for bit."""
+merge, and the channel aggregation with its dq partials. The only atomics
+are the dK/dV kernel's split key blocks (all of this shape's key blocks: two
+fp32 adds onto zero per element, which commute exactly), so two runs on the
+same inputs must agree bit for bit."""
 import numpy as np
 import pytest
 
