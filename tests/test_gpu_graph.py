@@ -72,3 +72,50 @@ def test_captured_step_replays_match_eager(store_ds):
     t.cuda.synchronize()
     for name, a, b in zip(("o", "lse", "dq", "dk", "dv"), (o, lse, dq, dk, dv), ref):
         assert t.equal(a, b), f"replay on new inputs: {name} differs from the eager call"
+
+
+_FIRST_CALL_CAPTURED = r"""
+import sys
+import numpy as np
+import torch
+sys.path.insert(0, sys.argv[1])
+sys.path.insert(0, sys.argv[1] + "/tests")
+import paper_2405_15780_amd as va
+import workloads
+from gpu_util import to_device
+B, H, N, d = 1, 3, 700, 96
+x = {n: to_device(a) for n, a in workloads.make_small_inputs(B, H, N, d, seed=6400).items()}
+f32 = dict(dtype=torch.float32, device="cuda")
+o, lse = torch.empty((B, H, N, d), **f32), torch.empty((B, H, N), **f32)
+grads = tuple(torch.empty((B, H, N, d), **f32) for _ in range(3))
+ws = torch.empty(va.workspace_bytes_kv(B, H, N, N, d, va.VITATTN_BWD_STORE_DS) // 4 + 64, **f32)
+va.fwd(x["q"], x["k"], x["v"], out=(o, lse))
+torch.cuda.synchronize()
+g = torch.cuda.CUDAGraph()
+with torch.cuda.graph(g):  # the process's first backward call
+    va.bwd(x["q"], x["k"], x["v"], o, lse, x["dout"], workspace=ws, out=grads, store_ds=True)
+for rep in range(2):
+    g.replay()
+    torch.cuda.synchronize()
+    ref = va.bwd(x["q"], x["k"], x["v"], o, lse, x["dout"], store_ds=True)
+    torch.cuda.synchronize()
+    for name, a, b in zip(("dq", "dk", "dv"), grads, ref):
+        assert torch.equal(a, b), (rep, name)
+print("first captured call ok", flush=True)
+"""
+
+
+def test_first_backward_call_inside_capture():
+    # The backward's launch looks up, once per device, how many dK/dV
+    # workgroups are resident at once (no stream work). In a fresh process the
+    # first call, and with it that lookup, happens during capture.
+    import os
+    import subprocess
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    print("case first backward call inside capture (child process)", flush=True)
+    r = subprocess.run([sys.executable, "-c", _FIRST_CALL_CAPTURED, root], capture_output=True, text=True,
+                       timeout=300)
+    print(r.stdout[-2000:], r.stderr[-2000:], flush=True)
+    assert r.returncode == 0 and "first captured call ok" in r.stdout
