@@ -40,7 +40,14 @@
  *  - Arguments are validated before anything is launched; on any error status
  *    no output is written and no kernel is enqueued. Validation itself makes
  *    no HIP call, so it works on a machine without a GPU.
- *  - Results are bitwise deterministic for identical inputs (no atomics).
+ *  - Results are bitwise deterministic for identical inputs on a given
+ *    device. The only atomics are in the dK/dV stage: when its last round of
+ *    key-block workgroups would be at most half full, those key blocks are
+ *    split over two workgroups (one per half of the query tiles) that add
+ *    into dK and dV rows zeroed first by the same call, and two fp32 adds
+ *    onto zero give the same bits in either order. Which blocks split
+ *    depends on the device's CU count, looked up once per device at the
+ *    first backward call (no stream work, so a graph capture may hold it).
  *  - Calls are thread-safe; concurrent calls on different streams are fine.
  */
 #ifndef VITATTN_H
