@@ -46,8 +46,13 @@
  *    split over two workgroups (one per half of the query tiles) that add
  *    into dK and dV rows zeroed first by the same call, and two fp32 adds
  *    onto zero give the same bits in either order. Which blocks split
- *    depends on the device's CU count, looked up once per device at the
- *    first backward call (no stream work, so a graph capture may hold it).
+ *    depends on the call's number of key blocks (B*H*ceil(N/128)) and the
+ *    device's CU count, looked up once per device at the first backward
+ *    call (no stream work, so a graph capture may hold it). A split key
+ *    block sums its query tiles in another order than a whole one, so the
+ *    same head's dk, dv can differ in the last bits between calls whose
+ *    grids split differently (a head alone against the same head among
+ *    others); within rounding they are the same.
  *  - Calls are thread-safe; concurrent calls on different streams are fine.
  */
 #ifndef VITATTN_H
