@@ -137,7 +137,7 @@ def test_one_million_tokens_sampled():
 
 
 def test_deterministic_and_head_slices_are_bitwise_equal():
-    # 6 x 6 key blocks in the full call and 6 per single-head call: both split
+    # 36 key blocks in the full call and 6 per single-head call: both split
     # every dK/dV key block over its two query halves (at most half a round of
     # workgroups), so the bits agree; where the two calls split different key
     # blocks dK and dV agree to rounding only
