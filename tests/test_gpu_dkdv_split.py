@@ -46,3 +46,26 @@ def test_split_key_blocks_are_deterministic():
     for a, b in ((runs[0], runs[1]), (runs[2], runs[3])):
         for name in ("dq", "dk", "dv"):
             assert t.equal(a[name], b[name]), name
+
+
+@pytest.mark.parametrize("store_ds", [False, True], ids=["recompute", "stored-ds"])
+def test_head_alone_and_among_others(store_ds):
+    # N = 25,600 gives 200 key blocks per head: a head alone is 200 work items
+    # (no split on a 256-CU part), three heads are 600 (the last 88, all of
+    # head 2, split). O, LSE and dQ do not depend on the split and stay
+    # bitwise equal; dK and dV of head 2 sum its query tiles in another order,
+    # so they agree to fp32 rounding.
+    t = torch()
+    B, H, N, d = 1, 3, 25600, 64
+    print(f"case head alone vs among others store_ds={store_ds}", flush=True)
+    x = workloads.make_small_inputs(B, H, N, d, seed=7801)
+    scale = 1.0 / np.sqrt(d)
+    full = run_hip(x, scale, store_ds=store_ds)
+    alone = run_hip({n: np.ascontiguousarray(a[:, 2:3]) for n, a in x.items()}, scale, store_ds=store_ds)
+    for name in ("o", "lse", "dq"):
+        assert t.equal(full[name][:, 2:3], alone[name]), name
+    for name in ("dk", "dv"):
+        a, b = full[name][:, 2:3].double(), alone[name].double()
+        rel = ((a - b).norm() / b.norm()).item()
+        print(f"{name}: rel L2 {rel:.2e}", flush=True)
+        assert rel < 1e-5, (name, rel)
