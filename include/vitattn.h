@@ -40,19 +40,19 @@
  *  - Arguments are validated before anything is launched; on any error status
  *    no output is written and no kernel is enqueued. Validation itself makes
  *    no HIP call, so it works on a machine without a GPU.
- *  - Results are bitwise deterministic for identical inputs on a given
- *    device. The only atomics are in the dK/dV stage: when its last round of
+ *  - Results are bitwise deterministic for identical inputs, and a head's
+ *    results do not depend on the call it is part of: one call over H heads
+ *    gives the bits of H single-head calls, whatever the grid or the CU
+ *    count. The only atomics are in the dK/dV stage: when its last round of
  *    key-block workgroups would be at most half full, those key blocks are
  *    split over two workgroups (one per half of the query tiles) that add
- *    into dK and dV rows zeroed first by the same call, and two fp32 adds
- *    onto zero give the same bits in either order. Which blocks split
- *    depends on the call's number of key blocks (B*H*ceil(N/128)) and the
- *    device's CU count, looked up once per device at the first backward
- *    call (no stream work, so a graph capture may hold it). A split key
- *    block sums its query tiles in another order than a whole one, so the
- *    same head's dk, dv can differ in the last bits between calls whose
- *    grids split differently (a head alone against the same head among
- *    others); within rounding they are the same.
+ *    into dK and dV rows zeroed first by the same call; two fp32 adds onto
+ *    zero give the same bits in either order. Every key block, split or
+ *    not, sums its query tiles as the same two rounded partial sums (split
+ *    at the middle query tile) and adds them, so splitting changes no bit.
+ *    Which blocks split depends on the number of key blocks (B*H*ceil(N/128))
+ *    and the device's CU count, looked up once per device at the first
+ *    backward call (no stream work, so a graph capture may hold it).
  *  - Calls are thread-safe; concurrent calls on different streams are fine.
  */
 #ifndef VITATTN_H
@@ -131,9 +131,8 @@ int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout
 /*
  * Attention over one segment of the keys, and the merge of such partial
  * results. Sequence parallelism over contiguous segments (Long Sequence
- * Segmentation, paper Sec. I and II "Sequence Parallel": each GPU computes a
- * partial self-attention for its segment) hands one GPU its queries and the
- * keys of one segment at a time. Softmax over a union of key sets factors
+ * Segmentation, paper Sec. I and II "Sequence Parallel"; one segment per
+ * worker) hands one GPU its queries and the keys of one segment at a time. Softmax over a union of key sets factors
  * over the sets:
  *
  *     LSE_i = log sum_s exp(LSE_s,i),   O_i = sum_s exp(LSE_s,i - LSE_i) O_s,i

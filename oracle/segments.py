@@ -1,11 +1,10 @@
 """Attention over key segments and the merge of the partial results, in fp64.
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
-Sequence parallelism that splits the sequence into contiguous segments (Long
-Sequence Segmentation, which the paper builds on in Sec. I and describes in
-Sec. II, "Sequence Parallel": each GPU computes a partial self-attention for
-its segment) leaves a worker with the attention of its queries over one
-segment of the keys at a time. Written
+Sequence parallelism over contiguous segments of the sequence (Long Sequence
+Segmentation, which the paper builds on in Sec. I and describes in Sec. II,
+"Sequence Parallel"; one segment per worker) leaves a worker with the
+attention of its queries over one segment of the keys at a time. Written
 from the definition of softmax over a union of key sets (LSE is the natural
 log of the summed exponentials of the scaled logits, as in the forward):
 

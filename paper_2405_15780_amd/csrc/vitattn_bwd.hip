@@ -113,7 +113,7 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 // round of them) are split into two workgroups each, one per half of the
 // query tiles, which add their dK and dV into rows the launch zeroed first.
 template <int D, bool STORE_DS>
-__global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
+__global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
     float* __restrict__ dk, float* __restrict__ dv, uint16_t* __restrict__ ds_out, const Map mq, const Map mk,
@@ -162,8 +162,16 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
     if (part & 1) t0 = n_qt_real >> 1;
     else t1 = n_qt_real >> 1;
   }
-  // query rows at or past qend read as zeros (the ragged end, or the other half's rows)
-  const int qend = min(Nq, t1 * kDkvBQ);
+  // Every key block sums its query tiles as two partial sums split at tile
+  // mid, each scaled and rounded on its own, then added: a split half adds
+  // its partial onto the zeroed row; a whole block runs the tile loop twice,
+  // over [0, mid) and [mid, n), storing the first partial in between and
+  // adding the second to it at the end. The two fp32 adds onto zero commute,
+  // so dK and dV have the same bits whether or not the grid splits the block
+  // (and so for any grid shape or CU count).
+  const int mid = n_qt_real >> 1;
+  const bool two_part = !split && mid > 0;
+  if (two_part) t1 = mid;
   const int bh = work / n_ktiles;
   const int kt = work - bh * n_ktiles;
   const int tid = threadIdx.x;
@@ -174,10 +182,15 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // queries, dO and the row statistics have Nq rows per (b, h); K, V, dK, dV have Nk
   const int chr = dr >> 3;  // 16-byte chunks of a row that hold data
   const int ldq = 2 * mq.ld, ldg = 2 * mg.ld;  // row strides in bytes
-  const rsrc_t rq = make_rsrc(q + mq.head(bh, H), (unsigned)(qend * ldq));
-  const rsrc_t rg = make_rsrc(dout + mg.head(bh, H), (unsigned)(qend * ldg));
-  const rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)qend * 4);
-  const rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)qend * 4);
+  // query rows at or past qend read as zeros (the ragged end, or rows of the
+  // other half or pass)
+  const uint16_t* const qh = q + mq.head(bh, H);
+  const uint16_t* const gh = dout + mg.head(bh, H);
+  int qend = min(Nq, t1 * kDkvBQ);
+  rsrc_t rq = make_rsrc(qh, (unsigned)(qend * ldq));
+  rsrc_t rg = make_rsrc(gh, (unsigned)(qend * ldg));
+  rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)qend * 4);
+  rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)qend * 4);
 
   // held fragments (B operands, columns = this block's keys): K for role P, V for role dS
   const int key = kt * kDkvBK + kb * 32 + (lane & 31);
@@ -203,6 +216,32 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   f32x16 acc[NCB];  // dV^T (role P) or dK^T (role dS)
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero16();
+
+  // Output row of this lane's key (dV for role P, dK for role dS) and the
+  // factor of its accumulator.
+  auto out_row = [&]() -> float* {
+    const Map& mout = role_p ? mdv : mdk;
+    return (role_p ? dv : dk) + mout.head(bh, H) + (size_t)key * mout.ld;
+  };
+  const float f = role_p ? 1.f : scale;
+  // Whole blocks, after their last tile below mid: store the first partial
+  // (rounded like the split halves' addends) and restart the sum.
+  auto store_first_part = [&]() __attribute__((always_inline)) {
+    if (key < Nk) {
+      float* out = out_row();
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int col = 32 * cb + 8 * g + 4 * h;
+          if (col < dr)
+            *reinterpret_cast<float4*>(out + col) = make_float4(acc[cb][4 * g] * f, acc[cb][4 * g + 1] * f,
+                                                                acc[cb][4 * g + 2] * f, acc[cb][4 * g + 3] * f);
+        }
+    }
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero16();
+  };
 
   // Tiles are numbered from t0 in the loops below. STORE_DS: the dS operands
   // of the wave's previous tile, not yet stored (padding tiles past t1 are not).
@@ -344,8 +383,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // Iteration t: role P on tile t (slot t % 3), role dS on tile t-1, tile t+1
   // requested into slot (t+1) % 3. Rounding the tile count to 1 mod 3 lets
   // iterations 1 .. n_pad-1 run in groups of three with fixed slots.
-  const int n_qt = t1 - t0;
-  const int n_pad = n_qt + (3 + 1 - n_qt % 3) % 3;
+  int n_pad = 0;
   // Each role runs its own copy of the tile loop, so that the compiler sees
   // in the dS waves' copy that (with STORE_DS) they never have a DMA request
   // in flight, and adds no wait for one; both copies pass the same barriers.
@@ -353,7 +391,8 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
   // with the slot refilled next. With STORE_DS the dS waves issued no loads
   // and skip the wait (their stores drain in the background); a plain
   // barrier then keeps the compiler from adding a wait for every access.
-  auto iteration = [&](auto role_tag, auto slot_p, auto slot_next, auto slot_ds, int t, bool run) {
+  auto iteration = [&](auto role_tag, auto slot_p, auto slot_next, auto slot_ds, int t, bool run)
+                       __attribute__((always_inline)) {
     constexpr bool RP = decltype(role_tag)::value;
     // tile t+1 past the end: zero rows, never read
     auto prefetch = [&]() {
@@ -374,7 +413,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       __syncthreads();
     }
   };
-  auto run_role = [&](auto role_tag) {
+  auto run_role = [&](auto role_tag) __attribute__((always_inline)) {
     constexpr bool RP = decltype(role_tag)::value;
     iteration(role_tag, S0{}, S1{}, S2{}, 0, RP);
     for (int t = 1; t < n_pad; t += 3) {
@@ -388,54 +427,98 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) void attn_bwd_dkdv_kernel(
       flush_ds();
     }
   };
-  if (!STORE_DS || role_p) issue_tile(S0{}, 0);
-  wait_vmem();
-  __syncthreads();
-  if constexpr (STORE_DS) {
-    if (role_p)
-      run_role(RoleP{});
-    else
-      run_role(RoleDs{});
-  } else {
-    // one loop for both roles (this form keeps the default kernel's register
-    // allocation; the role is a run-time branch inside each iteration)
-    auto both = [&](auto slot_p, auto slot_next, auto slot_ds, int t, bool do_p, bool do_ds) {
-      if (role_p) {
-        if (do_p) run_tile(RoleP{}, slot_p, t, [&]() { issue_tile(slot_next, t + 1); });
-        else issue_tile(slot_next, t + 1);
-      } else {
-        if (do_ds) run_tile(RoleDs{}, slot_ds, t - 1, [&]() { issue_tile(slot_next, t + 1); });
-        else issue_tile(slot_next, t + 1);
-      }
-      wait_vmem();
-      __syncthreads();
-    };
-    both(S0{}, S1{}, S2{}, 0, true, false);
-    for (int t = 1; t < n_pad; t += 3) {
-      both(S1{}, S2{}, S0{}, t, true, true);
-      both(S2{}, S0{}, S1{}, t + 1, true, true);
-      both(S0{}, S1{}, S2{}, t + 2, true, true);
+  // one loop for both roles (this form keeps the default kernel's register
+  // allocation; the role is a run-time branch inside each iteration)
+  auto both = [&](auto slot_p, auto slot_next, auto slot_ds, int t, bool do_p, bool do_ds)
+                  __attribute__((always_inline)) {
+    if (role_p) {
+      if (do_p) run_tile(RoleP{}, slot_p, t, [&]() { issue_tile(slot_next, t + 1); });
+      else issue_tile(slot_next, t + 1);
+    } else {
+      if (do_ds) run_tile(RoleDs{}, slot_ds, t - 1, [&]() { issue_tile(slot_next, t + 1); });
+      else issue_tile(slot_next, t + 1);
     }
-    if (!role_p) run_tile(RoleDs{}, S0{}, n_pad - 1, [] {});
+    wait_vmem();
+    __syncthreads();
+  };
+  const int n_pass = two_part ? 2 : 1;
+  // Whole block between its two passes: store the first partial, then move
+  // to the tiles [mid, n); every wave is done with the LDS ring and the P
+  // exchange before the next pass refills them.
+  auto next_pass = [&]() __attribute__((always_inline)) {
+    store_first_part();
+    t0 = mid;
+    t1 = n_qt_real;
+    qend = Nq;
+    rq = make_rsrc(qh, (unsigned)(qend * ldq));
+    rg = make_rsrc(gh, (unsigned)(qend * ldg));
+    rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)qend * 4);
+    rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)qend * 4);
+    wait_vmem();
+    __syncthreads();
+  };
+  auto start_pass = [&]() __attribute__((always_inline)) {
+    const int n_qt = t1 - t0;
+    n_pad = n_qt + (3 + 1 - n_qt % 3) % 3;
+    if (!STORE_DS || role_p) issue_tile(S0{}, 0);
+    wait_vmem();
+    __syncthreads();
+  };
+  if constexpr (STORE_DS) {
+    // each role runs its passes in its own branch (wave-uniform; both pass
+    // the same barriers), which keeps the dS waves' loop free of the other
+    // role's live values
+    if (role_p) {
+      for (int pass = 0; pass < n_pass; ++pass) {
+        start_pass();
+        run_role(RoleP{});
+        if (pass + 1 < n_pass) next_pass();
+      }
+    } else {
+      for (int pass = 0; pass < n_pass; ++pass) {
+        start_pass();
+        run_role(RoleDs{});
+        if (pass + 1 < n_pass) next_pass();
+      }
+    }
+  } else {
+    for (int pass = 0; pass < n_pass; ++pass) {
+      start_pass();
+      both(S0{}, S1{}, S2{}, 0, true, false);
+      for (int t = 1; t < n_pad; t += 3) {
+        both(S1{}, S2{}, S0{}, t, true, true);
+        both(S2{}, S0{}, S1{}, t + 1, true, true);
+        both(S0{}, S1{}, S2{}, t + 2, true, true);
+      }
+      if (!role_p) run_tile(RoleDs{}, S0{}, n_pad - 1, [] {});
+      if (pass + 1 < n_pass) next_pass();
+    }
   }
   (void)DMA_PER_TILE;
 
   if (key < Nk) {
-    const Map& mout = role_p ? mdv : mdk;
-    float* out = (role_p ? dv : dk) + mout.head(bh, H) + (size_t)key * mout.ld;
-    const float f = role_p ? 1.f : scale;
+    float* out = out_row();
+    if (two_part) wait_vmem();  // the first partial's stores have completed
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int col = 32 * cb + 8 * g + 4 * h;  // d is a multiple of 8: four columns are all in or all out
         if (col < dr) {
+          float x[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            x[e] = acc[cb][4 * g + e] * f;
+            pin(x[e]);  // rounded product, never fused into the add below
+          }
           if (split) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) unsafeAtomicAdd(out + col + e, acc[cb][4 * g + e] * f);
+            for (int e = 0; e < 4; ++e) unsafeAtomicAdd(out + col + e, x[e]);
+          } else if (two_part) {
+            const float4 a = *reinterpret_cast<const float4*>(out + col);
+            *reinterpret_cast<float4*>(out + col) = make_float4(a.x + x[0], a.y + x[1], a.z + x[2], a.w + x[3]);
           } else {
-            *reinterpret_cast<float4*>(out + col) = make_float4(acc[cb][4 * g] * f, acc[cb][4 * g + 1] * f,
-                                                                acc[cb][4 * g + 2] * f, acc[cb][4 * g + 3] * f);
+            *reinterpret_cast<float4*>(out + col) = make_float4(x[0], x[1], x[2], x[3]);
           }
         }
       }

@@ -1,6 +1,6 @@
 // Merge of partial attention results over key segments. Softmax over a union
-// of key sets factors over the sets (contiguous sequence segments, each GPU
-// computing a partial self-attention for its segment: paper Sec. I and II):
+// of key sets factors over the sets (contiguous key segments, one per
+// worker, as in the segment-based sequence parallelism of paper Sec. I and II):
 //
 //     LSE_i = log sum_s exp(LSE_s,i),   O_i = sum_s exp(LSE_s,i - LSE_i) O_s,i
 //

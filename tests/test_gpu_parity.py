@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import workloads
-from gpu_util import assert_close, run_hip, to_device, torch
+from gpu_util import assert_close, oracle_all_heads, run_hip, to_device, torch
 
 pytestmark = pytest.mark.gpu
 
@@ -88,17 +88,29 @@ _VIT_BLOCK_REF = {}
 
 
 @pytest.mark.parametrize("store_ds", [False, True], ids=["recompute", "stored-ds"])
-def test_vit_block_N16384_x8_head_full_heads_sampled_rows_and_identities(store_ds):
+def test_vit_block_N16384_x8_head_all_heads_full_compare(store_ds):
+    """The 16,384-token ViT block (B=2, H=16, d=64, head 0 of each batch with
+    Q and K scaled by 8) compared element by element in all five outputs for
+    every one of its 32 heads, plus the sampled-row and identity checks the
+    longer workloads use."""
     w = workloads.WORKLOADS[2]
     x = workloads.make_inputs(w)
     res = run_hip(x, w.scale, store_ds=store_ds)
-    heads = [(0, 0), (1, 7)]  # the x8 stress head and an ordinary one
     if "ref" not in _VIT_BLOCK_REF:  # the same seeded inputs in both modes
-        _VIT_BLOCK_REF["ref"] = oracle.forward_backward(x["q"], x["k"], x["v"], x["dout"], w.scale, heads=heads)
+        print(f"{w.name}: fp64 oracle over all {w.B * w.H} heads", flush=True)
+        _VIT_BLOCK_REF["ref"] = oracle_all_heads(x, w.scale)
     ref = _VIT_BLOCK_REF["ref"]
-    for b, h in heads:
-        got = {n: np64(t[b, h]) for n, t in res.items()}
-        assert_close(got, {n: a[b, h] for n, a in ref.items()}, label=f"{w.name} head ({b},{h})")
+    worst = {}
+    for b in range(w.B):
+        for h in range(w.H):
+            got = {n: np64(t[b, h]) for n, t in res.items()}
+            rep = assert_close(got, {n: a[b, h] for n, a in ref.items()}, label=f"{w.name} head ({b},{h})")
+            for key, val in rep.items():
+                if val > worst.get(key, (-1.0, None))[0]:
+                    worst[key] = (val, (b, h))
+    print(f"{w.name} worst over all heads:", {k: f"{v:.3e} at {bh}" for k, (v, bh) in worst.items()}, flush=True)
+    got = {n: np64(t) for n, t in res.items()}
+    assert_close(got, {n: ref[n] for n in got}, label=f"{w.name} all heads at once")
     _sampled_query_check(w, x, res, with_grad=True)
     _identities(w, x, res)
 
@@ -137,10 +149,9 @@ def test_one_million_tokens_sampled():
 
 
 def test_deterministic_and_head_slices_are_bitwise_equal():
-    # 36 key blocks in the full call and 6 per single-head call: both split
-    # every dK/dV key block over its two query halves (at most half a round of
-    # workgroups), so the bits agree; where the two calls split different key
-    # blocks dK and dV agree to rounding only
+    # one call over B*H heads against B*H single-head calls (Sec. VI-A checks
+    # that every process computes the same matrices): every output bitwise
+    # equal, whichever key blocks the dK/dV grid splits in either call
     B, H, N, d = 2, 3, 700, 128
     x = workloads.make_small_inputs(B, H, N, d, seed=5)
     scale = 1.0 / np.sqrt(d)
