@@ -70,7 +70,8 @@ enum vitattn_status {
   VITATTN_E_UNSUPPORTED = 2, /* head dim d not supported (see above) */
   VITATTN_E_WORKSPACE = 3,   /* workspace missing or smaller than vitattn_bwd_workspace_bytes() */
   VITATTN_E_HIP = 4,         /* the HIP runtime reported an error when launching */
-  VITATTN_E_INTERNAL = 5     /* unexpected internal failure */
+  VITATTN_E_INTERNAL = 5,    /* unexpected internal failure */
+  VITATTN_E_TOO_LARGE = 6    /* vitattn_bwd_noalloc only: B*H*N above VITATTN_NOALLOC_MAX_ROWS */
 };
 
 /*
@@ -318,6 +319,30 @@ size_t vitattn_agg_bwd_workspace_bytes(int M, int H, int C, int d);
 int vitattn_agg_bwd(const void* q, const void* k, const void* v, const float* o, const void* dout, const float* lse,
                     float* dq, float* dk, float* dv, int M, int H, int C, int d, float scale, void* workspace,
                     size_t workspace_bytes, void* stream);
+
+/*
+ * vitattn_bwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops that must not
+ * call hipMalloc, harnesses that forbid it). Same arguments (minus the
+ * workspace), layouts, validation, kernels and results as vitattn_bwd: the
+ * outputs are bitwise equal to vitattn_bwd's for the same inputs. The
+ * workspace lives in a static device array of the library (32 MiB, one copy
+ * per device the library runs on, held until the process ends), so:
+ *   - B*H*N may be at most VITATTN_NOALLOC_MAX_ROWS, else VITATTN_E_TOO_LARGE
+ *     (and nothing is launched);
+ *   - the call itself allocates nothing (no hipMalloc, hipFree or allocating
+ *     library routine). Its first call on a device looks up that device's
+ *     copy of the array (hipGetSymbolAddress) with that device current; the
+ *     stream must belong to the calling thread's current device;
+ *   - every call on a device shares that device's array: calls that overlap
+ *     in time on one device (other streams, other threads) race and must be
+ *     serialised by the caller. Nothing in the array needs clearing between
+ *     calls: each call rewrites every entry it reads.
+ */
+#define VITATTN_NOALLOC_MAX_ROWS 4194304
+int vitattn_bwd_noalloc(const void* q, const void* k, const void* v, const float* o, const void* dout,
+                        const float* lse, float* dq, float* dk, float* dv, int B, int H, int N, int d, float scale,
+                        void* stream);
 
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* vitattn_status_str(int status);

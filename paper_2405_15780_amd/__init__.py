@@ -10,6 +10,7 @@ from .binding import (  # noqa: F401
     LIB_PATH,
     VITATTN_BWD_ACCUMULATE_DQ,
     VITATTN_BWD_STORE_DS,
+    VITATTN_NOALLOC_MAX_ROWS,
     Strides,
     VitattnError,
     agg_bwd,
@@ -19,6 +20,7 @@ from .binding import (  # noqa: F401
     bwd_dkdv_ds,
     bwd_dq,
     bwd_dq_from_ds,
+    bwd_noalloc,
     bwd_rowdot,
     fwd,
     library,

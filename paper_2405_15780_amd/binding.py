@@ -50,6 +50,7 @@ _SIGNATURES = {
     "vitattn_ulysses_unpack": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
     "vitattn_ulysses_pack_out": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
     "vitattn_ulysses_unpack_out": (c_int, [c_void_p] * 2 + [c_int] * 5 + [c_void_p]),
+    "vitattn_bwd_noalloc": (c_int, [c_void_p] * 9 + [c_int] * 4 + [c_float, c_void_p]),
     "vitattn_status_str": (ctypes.c_char_p, [c_int]),
     "vitattn_version": (ctypes.c_char_p, []),
 }
@@ -254,6 +255,33 @@ def bwd(q, k, v, o, lse, dout, scale=None, workspace=None, out=None, accumulate_
                                 lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, Nq, Nk, d,
                                 _default_scale(d, scale), flags, ws.data_ptr(), ws_bytes, _stream_ptr(q))
     _check(st)
+    return dq, dk, dv
+
+
+VITATTN_NOALLOC_MAX_ROWS = 4194304
+
+
+def bwd_noalloc(q, k, v, o, lse, dout, scale=None, out=None):
+    """The backward pass through vitattn_bwd_noalloc (no workspace: the
+    library's static scratch; B*H*N at most VITATTN_NOALLOC_MAX_ROWS; calls on
+    one device must not overlap). Dense [B,H,N,d] operands; out=(dq, dk, dv)
+    to write into existing tensors."""
+    torch = _torch()
+    B, H, N, d = _shape4(q, "q")
+    dev = q.device
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (dout, "dout")):
+        _expect(t, n, torch.bfloat16, (B, H, N, d), dev, dense=True)
+    _expect(o, "o", torch.float32, (B, H, N, d), dev, dense=True)
+    _expect(lse, "lse", torch.float32, (B, H, N), dev, dense=True)
+    if out is None:
+        dq, dk, dv = (torch.empty((B, H, N, d), dtype=torch.float32, device=dev) for _ in range(3))
+    else:
+        dq, dk, dv = out
+        for t, n in ((dq, "dq"), (dk, "dk"), (dv, "dv")):
+            _expect(t, n, torch.float32, (B, H, N, d), dev, dense=True)
+    _check(library().vitattn_bwd_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), dout.data_ptr(),
+                                         lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, N, d,
+                                         _default_scale(d, scale), _stream_ptr(q)))
     return dq, dk, dv
 
 

@@ -6,6 +6,7 @@
 #include <stdlib.h>
 
 #include <exception>
+#include <mutex>
 
 #include "../../include/vitattn.h"
 #include "vitattn_launch.h"
@@ -99,6 +100,8 @@ const char* vitattn_status_str(int status) {
     case VITATTN_E_WORKSPACE: return "VITATTN_E_WORKSPACE: workspace missing or too small";
     case VITATTN_E_HIP: return "VITATTN_E_HIP: HIP runtime error at launch";
     case VITATTN_E_INTERNAL: return "VITATTN_E_INTERNAL: internal error";
+    case VITATTN_E_TOO_LARGE:
+      return "VITATTN_E_TOO_LARGE: B*H*N exceeds VITATTN_NOALLOC_MAX_ROWS, the static scratch of vitattn_bwd_noalloc";
     default: return "VITATTN: unknown status";
   }
 }
@@ -449,6 +452,68 @@ int vitattn_agg_bwd(const void* q, const void* k, const void* v, const float* o,
     a.scale = scale;
     a.stream = static_cast<hipStream_t>(stream);
     return vitattn::launch_agg_bwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
+  } catch (...) {
+    return VITATTN_E_INTERNAL;
+  }
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------ allocation-free backward
+//
+// The backward pass's only scratch memory is its workspace: the row statistic
+// D and LSE*log2(e), one float each per query row. vitattn_bwd_noalloc keeps
+// them in this file-scope array instead of a caller's buffer, sized for
+// VITATTN_NOALLOC_MAX_ROWS rows (32 MiB; every device the library runs on
+// holds its own copy until the process ends). In host code `scratch` names a
+// host-side stand-in, not device memory: kernels get the device address that
+// hipGetSymbolAddress returns, looked up once per device with that device
+// current. Every call on a device shares that device's copy, and the row
+// kernel rewrites every row the later kernels read, so nothing is cleared
+// between calls; calls that overlap on one device race.
+namespace {
+// D and LSE*log2(e), each region padded like the workspace (bwd_region_floats)
+constexpr size_t kNoAllocScratchFloats = 2 * (((size_t)VITATTN_NOALLOC_MAX_ROWS + 63) / 64 * 64);
+static_assert(kNoAllocScratchFloats * sizeof(float) == (32u << 20), "32 MiB of scratch");
+constexpr int kMaxDevices = 64;
+}  // namespace
+
+static __device__ __align__(256) float scratch[kNoAllocScratchFloats];
+
+// Device address of this device's copy of `scratch` (nullptr on a HIP error).
+static void* noalloc_scratch() {
+  static std::mutex mu;
+  static void* ptrs[kMaxDevices] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (ptrs[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    ptrs[dev] = p;
+  }
+  return ptrs[dev];
+}
+
+extern "C" {
+
+int vitattn_bwd_noalloc(const void* q, const void* k, const void* v, const float* o, const void* dout,
+                        const float* lse, float* dq, float* dk, float* dv, int B, int H, int N, int d, float scale,
+                        void* stream) {
+  try {
+    int st = check_sizes(B, H, N, d);
+    if (st != VITATTN_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(lse) ||
+        !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+      return VITATTN_E_INVAL;
+    if (!scale_ok(scale)) return VITATTN_E_INVAL;
+    const long long rows = (long long)B * H * N;
+    if (rows > VITATTN_NOALLOC_MAX_ROWS) return VITATTN_E_TOO_LARGE;
+    void* ws = noalloc_scratch();
+    if (ws == nullptr) return VITATTN_E_HIP;
+    const vitattn::BwdArgs a =
+        bwd_args(q, k, v, o, dout, lse, dq, dk, dv, B, H, N, N, d, scale, false, ws, stream);
+    return vitattn::launch_bwd(a) == hipSuccess ? VITATTN_OK : VITATTN_E_HIP;
   } catch (...) {
     return VITATTN_E_INTERNAL;
   }

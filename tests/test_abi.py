@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_status_strings_and_version():
     assert va.version() == "0.3.0"
-    for s in range(6):
+    for s in range(7):
         assert va.status_str(s).startswith("VITATTN")
     assert "unknown" in va.status_str(99)
 
@@ -134,6 +134,26 @@ def test_bwd_rejects_null_pointers(which):
     assert bwd(b, override={which: None}) == E_INVAL
     assert bwd(b, override={which: b.p(which) + 4}) == E_INVAL
     assert b.untouched()
+
+
+def noalloc(b, B=1, H=1, N=8, d=64, scale=0.125, override=None):
+    ptrs = [b.p(i) for i in range(9)]
+    for i, val in (override or {}).items():
+        ptrs[i] = val
+    return lib().vitattn_bwd_noalloc(*ptrs, B, H, N, d, scale, None)
+
+
+@pytest.mark.parametrize("kw,expected", [
+    (dict(N=0), E_INVAL), (dict(d=84), E_UNSUP), (dict(scale=float("nan")), E_INVAL),
+    (dict(override={3: None}), E_INVAL), (dict(override={8: 12346}), E_INVAL),
+    # one row past the static scratch, and the same rows as B*H*N in another split
+    (dict(N=va.VITATTN_NOALLOC_MAX_ROWS + 1), 6), (dict(B=2, H=2, N=va.VITATTN_NOALLOC_MAX_ROWS // 4 + 1), 6),
+])
+def test_bwd_noalloc_rejects_bad_arguments_before_any_hip_call(kw, expected):
+    b = Bufs()
+    assert noalloc(b, **kw) == expected
+    assert b.untouched()
+    assert "VITATTN_NOALLOC_MAX_ROWS" in va.status_str(6)
 
 
 def test_bwd_stages_validate():
