@@ -43,9 +43,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 512 MiB device copy (to scale rocprofv3 FETCH_SIZE/WRITE_SIZE)")
-    p.add_argument("--bwd-mode", choices=["auto", "recompute", "stored-ds"], default="auto",
-                   help="backward pass of the default workload: recompute S and dP for dQ, or dQ from the dS "
-                        "blocks the dK/dV kernel stores (a B*H*N^2*2-byte workspace); auto = stored-ds when it fits")
+    p.add_argument("--bwd-mode", choices=["recompute", "stored-ds"], default="recompute",
+                   help="backward pass: recompute (the default: dQ recomputes S and dP, O(N d) memory), or "
+                        "stored-ds (opt-in: dQ from the dS blocks the dK/dV kernel stores, a B*H*N^2*2-byte "
+                        "workspace, 142 GB at the 188,416-token workload)")
     p.add_argument("--hbm-reference", action="store_true",
                    help="only measure the streaming rates of plain elementwise kernels (read+write, "
                         "read 1 : write 2, write only)")
@@ -286,23 +287,37 @@ def cpu_baseline(w, x, budget_s):
         threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     except Exception:  # threadpoolctl missing: report the BLAS default
         threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    # blocks of up to 512 query rows in workload order (b, h, rows), each
+    # against all N keys of its head; a workload smaller than the budget is
+    # gone through again from the start
     rows_per_block = 512
-    done = 0
+    blocks = [(b, h, r0) for b in range(w.B) for h in range(w.H) for r0 in range(0, w.N, rows_per_block)]
+    done = n_blocks = 0
     t0 = time.perf_counter()
-    while done < w.N and time.perf_counter() - t0 < budget_s:
-        r1 = min(w.N, done + rows_per_block)
-        oracle.forward_backward_rows(x["q"], x["k"], x["v"], x["dout"], w.scale, 0, 0, done, r1)
-        done = r1
+    while n_blocks == 0 or time.perf_counter() - t0 < budget_s:
+        b, h, r0 = blocks[n_blocks % len(blocks)]
+        r1 = min(w.N, r0 + rows_per_block)
+        if w.backward:
+            oracle.forward_backward_rows(x["q"], x["k"], x["v"], x["dout"], w.scale, b, h, r0, r1)
+        else:
+            rows = np.stack([np.full(r1 - r0, b, np.int64), np.full(r1 - r0, h, np.int64),
+                             np.arange(r0, r1, dtype=np.int64)], axis=1)
+            oracle.query_rows(x["q"], x["k"], x["v"], w.scale, rows)
+        done += r1 - r0
+        n_blocks += 1
     dt = time.perf_counter() - t0
     flops = 14.0 * done * w.N * w.d if w.backward else 4.0 * done * w.N * w.d
     rows_total = w.B * w.H * w.N
+    passes = "forward+backward" if w.backward else "forward"
+    covered = (f"the first {done} of the workload's {rows_total} query rows" if n_blocks <= len(blocks) else
+               f"all {rows_total} query rows of the workload, {done / rows_total:.1f} times over")
     return {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"fp64 forward+backward of query rows 0..{done - 1} of head 0 against all {w.N} keys "
-                  f"({done}/{w.B * w.H * w.N} of the workload's rows), {dt:.1f} s",
+        "sample": f"fp64 {passes} of {covered} (blocks of {rows_per_block} rows in (b, h, row) order), each "
+                  f"against all {w.N} keys of its head, {dt:.1f} s",
         "seconds": dt,
         "extrapolated_full_seconds": dt * rows_total / done,
         "extrapolated": "per-row time of the sample times all B*H*N query rows (labelled extrapolated, not run)",
@@ -599,7 +614,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w = workloads.WORKLOADS[args.workload]
     B, H, N, d = w.shape
-    x = workloads.make_inputs(w, with_dout=True)
+    x = workloads.make_inputs(w)
     dev = torch.device("cuda:0")
     t = {n: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev) for n, a in x.items()}
     f32 = dict(dtype=torch.float32, device=dev)
@@ -607,15 +622,17 @@ def main():
     lse = torch.empty((B, H, N), **f32)
     dq, dk, dv = (torch.empty((B, H, N, d), **f32) for _ in range(3))
     scale = w.scale
-    # backward mode: the dS mode needs B*H*N^2*2 bytes of workspace (142 GB here)
+    # backward mode: recompute (O(N d) memory) unless the opt-in dS mode is
+    # asked for, which needs B*H*N^2*2 bytes of workspace (142 GB at N=188,416)
     ds_bytes = va.workspace_bytes_kv(B, H, N, N, d, va.VITATTN_BWD_STORE_DS)
     free_bytes = torch.cuda.mem_get_info(dev)[0]
     fits = ds_bytes > 0 and ds_bytes + (8 << 30) < free_bytes
-    mode = args.bwd_mode if args.bwd_mode != "auto" else ("stored-ds" if fits and w.backward else "recompute")
+    mode = args.bwd_mode if w.backward else "none"
     if mode == "stored-ds" and not fits:
         print(json.dumps({"error": f"the dS-mode workspace ({ds_bytes / 1e9:.0f} GB) does not fit"}))
         sys.exit(2)
     ws = torch.empty(max(ds_bytes if mode == "stored-ds" else va.workspace_bytes(B, H, N, d), 4) // 4, **f32)
+    workspace_gb = ws.numel() * 4 / 1e9  # of the timed mode (the comparison below may enlarge ws)
 
     def step(ev=None, m=None):
         m = m or mode
@@ -713,6 +730,7 @@ def main():
         torch.cuda.synchronize()
         alt_ms = float(np.mean([e[0].elapsed_time(e[4]) for e in ev2]))
         alt = {"bwd_mode": other, "ms_per_step": alt_ms, "value": flops["total"] / (alt_ms * 1e-3) / 1e12,
+               "workspace_gb": (ds_bytes if other == "stored-ds" else va.workspace_bytes(B, H, N, d)) / 1e9,
                "kernels_ms": {n: float(np.mean([e[spans[n][0]].elapsed_time(e[spans[n][1]]) for e in ev2]))
                               for n in names}}
 
@@ -734,8 +752,13 @@ def main():
         # peak at the clock the chip actually held: 256 CU x 4096 flop/clk x sclk
         peak_at_sclk = 256 * 4096 * smi_summary["sclk_mhz_median"] * 1e6 / 1e12
         clock = dict(smi_summary, peak_tflops_at_sclk=peak_at_sclk, pct_of_peak_at_sclk=100.0 * value / peak_at_sclk)
+    if args.workload == 4:
+        metric = "attention fwd+bwd TFLOP/s and % of bf16 MFMA peak at N=188,416, d=128"
+    else:
+        metric = (f"attention {'fwd+bwd' if w.backward else 'fwd'} TFLOP/s and % of bf16 MFMA peak, "
+                  f"B={B}, H={H}, N={N:,}, d={d}")
     result = {
-        "metric": "attention fwd+bwd TFLOP/s and % of bf16 MFMA peak at N=188,416, d=128",
+        "metric": metric,
         "value": value,
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -749,7 +772,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": B, "H": H, "N": N, "d": d, "passes": "fwd+bwd" if w.backward else "fwd",
                    "grid": f"{w.grid[0]}x{w.grid[1]}", "seed": w.seed, "bwd_mode": mode,
-                   "workspace_gb": ws.numel() * 4 / 1e9},
+                   "workspace_gb": workspace_gb},
         "other_bwd_mode": alt,
         "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "counted_tflop_per_step": flops["total"] / 1e12,

@@ -36,8 +36,10 @@
 // The row sum adds the fp32 probabilities in two partial sums (plain adds:
 // a v_dot2 over the bf16 pairs would compete with the matrix cores). The
 // rescale of O by exp2(m_old - m_new) is skipped when no query of the wave
-// raised its running max (multiplying by 1 would change nothing), so the
-// maximum is always subtracted exactly and the largest P is exactly 1.
+// raised its running max (multiplying by 1 would change nothing). The
+// running max m is kept pre-multiplied by the scale (m = fl(max * c)) and
+// subtracted inside one FMA, exp2(fma(s, c, -m)), so the largest P is 1 up
+// to the rounding of that product (one fp32 ulp of the scaled logit).
 #include <type_traits>
 
 #include "vitattn_common.h"
@@ -118,7 +120,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
 #pragma unroll
   for (int cb = 0; cb < D / 32; ++cb) oacc[cb] = zero16();
   float m_run = -INFINITY;  // running max of scaled logits, log2 units
-  float l_part = 0.f;       // this lane's share of the sum of the bf16 probabilities
+  float l_part = 0.f;       // this lane's share of the sum of the fp32 probabilities
 
   const int n_kt = (Nk + BN - 1) / BN;
   dma.issue(rk, 0, ldk, kbuf[0]);
