@@ -63,7 +63,7 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __
 
 // ------------------------------------------------------------------ dK / dV
 
-constexpr int kDkvBK = 32 * kBwdWaves;  // keys per workgroup
+constexpr int kDkvBK = 32 * kBwdWaves;  // keys per workgroup (KBW = kBwdWaves key blocks)
 constexpr int kDkvBQ = 64;              // queries per streamed tile
 constexpr int kDkvAhead = 2;            // LDS operand reads this many matrix-core ops ahead (3 measured no better)
 
@@ -76,13 +76,14 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_void_t*)(lds_stats + kDkvBQ), 4, (row0 + lane) * 4, 0, 0, 0);
 }
 
-// One workgroup = 8 waves = 128 keys of one (b, h), in four blocks of 32
-// keys. Each key block has two waves with split roles (waves w and w+4 share
-// a SIMD, so their vector and matrix phases interleave):
-//   role P  (waves 0-3): holds K, accumulates dV^T.
+// One workgroup = 2*KBW waves = 32*KBW keys of one (b, h), in KBW blocks of
+// 32 keys (KBW = 4: 8 waves, 128 keys; 6 at the narrowest tile: 12 waves).
+// Each key block has two waves with split roles (waves share the SIMDs round
+// robin, so the vector and matrix phases of the roles interleave):
+//   role P  (waves 0 .. KBW-1): holds K, accumulates dV^T.
 //     S = Q K^T;  P = exp2(S*scale*log2e - LSE2);  dV^T += dO^T P;
 //     writes P (bf16) to LDS for its partner.
-//   role dS (waves 4-7): holds V, accumulates dK^T, one tile behind.
+//   role dS (waves KBW .. 2*KBW-1): holds V, accumulates dK^T, one tile behind.
 //     dP = dO V^T;  dS = P o (dP - D) with the partner's P;  dK^T += Q^T dS.
 // Q, dO and the row statistics stream through a ring of three LDS slots in
 // tiles of 64 queries (two blocks of 32); in iteration t role P works on
@@ -112,8 +113,8 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 // own a key block and every query; the key blocks after them (at most half a
 // round of them) are split into two workgroups each, one per half of the
 // query tiles, which add their dK and dV into rows the launch zeroed first.
-template <int D, bool STORE_DS>
-__global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_bwd_dkdv_kernel(
+template <int D, bool STORE_DS, int KBW>
+__global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per_eu(KBW / 2, KBW / 2))) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
     float* __restrict__ dk, float* __restrict__ dv, uint16_t* __restrict__ ds_out, const Map mq, const Map mk,
@@ -125,7 +126,8 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per
   // query rows of vector work: row r rides on op slot r * PH / 16 of its phase
   constexpr int TILE_BYTES = kDkvBQ * D * 2;
   constexpr int RING = 3;
-  constexpr int NWAVES = 2 * kBwdWaves;
+  constexpr int NWAVES = 2 * KBW;
+  constexpr int BK = 32 * KBW;  // keys per workgroup
   // One variable per ring slot: the compiler then knows that reading one
   // slot never overlaps the DMA into another and inserts no wait for it.
   __shared__ __attribute__((aligned(1024))) char qbuf0[TILE_BYTES];
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per
   // the narrower tiles use the ring slot instead, a compile-time index. The
   // widest tile needs the two-slot form to fit in LDS.
   constexpr int XR = D == 160 ? 2 : RING;
-  __shared__ __attribute__((aligned(16))) uint4 xbuf[XR][kBwdWaves][2][2][64];
+  __shared__ __attribute__((aligned(16))) uint4 xbuf[XR][KBW][2][2][64];
   debug_poison_lds(qbuf0, qbuf1, qbuf2, gbuf0, gbuf1, gbuf2, sbuf0, sbuf1, sbuf2, xbuf);
 
   // this workgroup's key block (work item) and query tiles [t0, t1)
@@ -176,8 +178,8 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per
   const int kt = work - bh * n_ktiles;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, h = lane >> 5;
-  const int kb = wave & 3;
-  const bool role_p = wave < 4;
+  const int kb = wave % KBW;
+  const bool role_p = wave < KBW;
 
   // queries, dO and the row statistics have Nq rows per (b, h); K, V, dK, dV have Nk
   const int chr = dr >> 3;  // 16-byte chunks of a row that hold data
@@ -193,7 +195,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per
   rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)qend * 4);
 
   // held fragments (B operands, columns = this block's keys): K for role P, V for role dS
-  const int key = kt * kDkvBK + kb * 32 + (lane & 31);
+  const int key = kt * BK + kb * 32 + (lane & 31);
   const Map& mh = role_p ? mk : mv;
   const int ldh = 2 * mh.ld;
   const rsrc_t rh = make_rsrc((role_p ? k : v) + mh.head(bh, H), (unsigned)(Nk * ldh));
@@ -203,7 +205,7 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per
 
   // Q and dO tiles. With STORE_DS only the four role-P waves fetch tiles, so
   // the dS waves never wait for a DMA request (and with it, for their stores).
-  constexpr int DMA_WAVES = STORE_DS ? kBwdWaves : NWAVES;
+  constexpr int DMA_WAVES = STORE_DS ? KBW : NWAVES;
   TileDma<D, kDkvBQ, DMA_WAVES> dma, dmg;
   dma.init(wave % DMA_WAVES, lane, ldq, chr);
   dmg.init(wave % DMA_WAVES, lane, ldg, chr);
@@ -251,9 +253,9 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per
     if constexpr (STORE_DS) {
       if (pend_tile >= 0 && pend_tile < t1 - t0) {
         // blocks (key block, query blocks 2t and 2t+1) of this head, 2 KB each
-        const size_t nkb = (size_t)n_ktiles * kBwdWaves, nqb = 2 * (size_t)n_qt_real;
+        const size_t nkb = (size_t)n_ktiles * KBW, nqb = 2 * (size_t)n_qt_real;
         uint16_t* dst =
-            ds_out + (((size_t)bh * nkb + (size_t)kt * kBwdWaves + kb) * nqb + 2 * (size_t)(t0 + pend_tile)) * 1024;
+            ds_out + (((size_t)bh * nkb + (size_t)kt * KBW + kb) * nqb + 2 * (size_t)(t0 + pend_tile)) * 1024;
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
@@ -530,13 +532,13 @@ __global__ __launch_bounds__(2 * kBwdThreads, 2) __attribute__((amdgpu_waves_per
 // split workgroups then add into.
 __global__ __launch_bounds__(256) void zero_key_blocks_kernel(float* __restrict__ dk, float* __restrict__ dv,
                                                               const Map mdk, const Map mdv, int H, int dr, int Nk,
-                                                              int n_ktiles, int first) {
+                                                              int n_ktiles, int first, int bk) {
   const int work = first + (blockIdx.x >> 1);
   const bool is_v = blockIdx.x & 1;
   const int bh = work / n_ktiles, kt = work - bh * n_ktiles;
   const Map& m = is_v ? mdv : mdk;
   float* base = (is_v ? dv : dk) + m.head(bh, H);
-  const int c4 = dr >> 2, key0 = kt * kDkvBK, rows = min(kDkvBK, Nk - key0);
+  const int c4 = dr >> 2, key0 = kt * bk, rows = min(bk, Nk - key0);
   for (int i = threadIdx.x; i < rows * c4; i += 256) {
     const int r = i / c4, c = i - r * c4;
     *reinterpret_cast<float4*>(base + (long long)(key0 + r) * m.ld + 4 * c) = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -558,7 +560,7 @@ __global__ __launch_bounds__(256) void zero_key_blocks_kernel(float* __restrict_
 // past the end arrive as zeros: their P is finite and they add
 // K_row^T dS = 0 to dQ, so no masking is needed.
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW, 2) void attn_bwd_dq_kernel(
+__global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4))) void attn_bwd_dq_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
     float* __restrict__ dq, const Map mq, const Map mk, const Map mv, const Map mg, const Map mdq, int H, int dr,
@@ -960,7 +962,7 @@ static hipError_t rowdot_l(const BwdArgs& a) {
 
 // Workgroups of the dK/dV kernel resident on the current device at once
 // (0 if the runtime cannot say), looked up once per device.
-template <int D, bool STORE_DS>
+template <int D, bool STORE_DS, int KBW>
 static int dkdv_resident_workgroups() {
   static std::atomic<int> known[64];  // per device ordinal; 0 = not looked up, -1 = unknown
   int dev = 0;
@@ -969,7 +971,7 @@ static int dkdv_resident_workgroups() {
   if (n == 0) {
     int per_cu = 0, cus = 0;
     n = -1;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dkdv_kernel<D, STORE_DS>, 2 * kBwdThreads,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dkdv_kernel<D, STORE_DS, KBW>, 128 * KBW,
                                                      0) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && per_cu * cus > 0)
       n = per_cu * cus;
@@ -978,45 +980,52 @@ static int dkdv_resident_workgroups() {
   return n > 0 ? n : 0;
 }
 
-template <int D, bool STORE_DS>
+template <int D, bool STORE_DS, int KBW>
 static hipError_t dkdv_s(const BwdArgs& a) {
-  const int n_kt = (a.Nk + kDkvBK - 1) / kDkvBK;
+  constexpr int BK = 32 * KBW;
+  const int n_kt = (a.Nk + BK - 1) / BK;
   const int total = a.BH * n_kt;
   // A last round at most half full is split in two halves of the query range
   // (when there are two query tiles to split), so that it takes half as long.
-  const int slots = dkdv_resident_workgroups<D, STORE_DS>();
+  const int slots = dkdv_resident_workgroups<D, STORE_DS, KBW>();
   const int tail = slots > 0 ? total % slots : 0;
   int n_whole = total;
   if (tail > 0 && 2 * tail <= slots && (a.Nq + kDkvBQ - 1) / kDkvBQ >= 2) {
     n_whole = total - tail;
     hipLaunchKernelGGL(zero_key_blocks_kernel, dim3(2 * tail), dim3(256), 0, a.stream, a.dk, a.dv, a.mdk, a.mdv, a.H,
-                       a.d, a.Nk, n_kt, n_whole);
+                       a.d, a.Nk, n_kt, n_whole, BK);
   }
   const int grid = n_whole + 2 * (total - n_whole);
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS>), dim3(grid), dim3(2 * kBwdThreads), 0, a.stream, a.q,
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS, KBW>), dim3(grid), dim3(64 * 2 * KBW), 0, a.stream, a.q,
                      a.k, a.v, a.dout, a.drow, a.lse2, a.dk, a.dv, a.ds, a.mq, a.mk, a.mv, a.mg, a.mdk, a.mdv, a.H,
                      a.d, a.Nq, a.Nk, n_kt, n_whole, a.scale * kLog2e, a.scale);
   return hipGetLastError();
 }
+// Key blocks of 32 per workgroup (two waves each): four, except at the
+// narrowest tile in the recompute mode, whose 166 VGPRs leave room for three
+// waves per SIMD: six key blocks (12 waves, 192 keys) stream each Q / dO tile
+// to half again as many keys. The dS mode keeps four (its stored dS blocks are
+// laid out per 128 keys).
 template <int D>
 static hipError_t dkdv_d(const BwdArgs& a) {
-  return a.ds != nullptr ? dkdv_s<D, true>(a) : dkdv_s<D, false>(a);
+  if (a.ds != nullptr) return dkdv_s<D, true, 4>(a);
+  return dkdv_s<D, false, D == 64 ? 6 : 4>(a);
 }
 
-#define VITATTN_DKDV_INSTANTIATE(D, S)                                                                         \
-  template __global__ void attn_bwd_dkdv_kernel<D, S>(                                                        \
+#define VITATTN_DKDV_INSTANTIATE(D, S, KBW)                                                                    \
+  template __global__ void attn_bwd_dkdv_kernel<D, S, KBW>(                                                   \
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
       float* __restrict__, uint16_t* __restrict__, const Map, const Map, const Map, const Map, const Map,      \
       const Map, int, int, int, int, int, int, float, float);
-VITATTN_DKDV_INSTANTIATE(128, false)
-VITATTN_DKDV_INSTANTIATE(64, false)
-VITATTN_DKDV_INSTANTIATE(96, false)
-VITATTN_DKDV_INSTANTIATE(160, false)
-VITATTN_DKDV_INSTANTIATE(128, true)
-VITATTN_DKDV_INSTANTIATE(64, true)
-VITATTN_DKDV_INSTANTIATE(96, true)
-VITATTN_DKDV_INSTANTIATE(160, true)
+VITATTN_DKDV_INSTANTIATE(128, false, 4)
+VITATTN_DKDV_INSTANTIATE(64, false, 6)
+VITATTN_DKDV_INSTANTIATE(96, false, 4)
+VITATTN_DKDV_INSTANTIATE(160, false, 4)
+VITATTN_DKDV_INSTANTIATE(128, true, 4)
+VITATTN_DKDV_INSTANTIATE(64, true, 4)
+VITATTN_DKDV_INSTANTIATE(96, true, 4)
+VITATTN_DKDV_INSTANTIATE(160, true, 4)
 #undef VITATTN_DKDV_INSTANTIATE
 
 template <int D, int NW, int RING>
@@ -1062,6 +1071,7 @@ static hipError_t dq_v(const BwdArgs& a) {
       const Map, const Map, const Map, const Map, const Map, int, int, int, int, int, int, float, float, int);
 VITATTN_DQ_INSTANTIATE(128, 8)
 VITATTN_DQ_INSTANTIATE(64, 8)
+VITATTN_DQ_INSTANTIATE(64, 12)
 VITATTN_DQ_INSTANTIATE(96, 8)
 VITATTN_DQ_INSTANTIATE(160, 8)
 #undef VITATTN_DQ_INSTANTIATE
@@ -1086,10 +1096,44 @@ hipError_t launch_bwd_dq_ds(const BwdArgs& a) {
     default: return dq_ds_d<160>(a);
   }
 }
+// Workgroups of a dQ kernel variant resident on the current device at once
+// (0 if the runtime cannot say), looked up once per device.
+template <int D, int NW>
+static int dq_resident_workgroups() {
+  static std::atomic<int> known[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int n = known[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    int per_cu = 0, cus = 0;
+    n = -1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dq_kernel<D, NW>, 64 * NW, 0) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && per_cu * cus > 0)
+      n = per_cu * cus;
+    known[dev].store(n, std::memory_order_relaxed);
+  }
+  return n > 0 ? n : 0;
+}
+
+// At the narrowest tile the dQ kernel's 168 VGPRs fit three waves per SIMD:
+// 12 waves (384 queries) per workgroup share each K / V tile, ~6 % faster per
+// query than 8 waves (measured at B=4, H=1, N=188,416), but in coarser work
+// items. The variant with the shorter estimated time (whole rounds of
+// resident workgroups x queries per workgroup / that rate) is launched; both
+// compute every dQ row with the same operations in the same order, so the
+// choice changes no bit.
+static hipError_t dq_64(const BwdArgs& a) {
+  const int s8 = dq_resident_workgroups<64, 8>(), s12 = dq_resident_workgroups<64, 12>();
+  if (s8 <= 0 || s12 <= 0) return dq_v<64, 8>(a);
+  const long long t8 = (long long)a.BH * ((a.Nq + 255) / 256), t12 = (long long)a.BH * ((a.Nq + 383) / 384);
+  const double c8 = (double)((t8 + s8 - 1) / s8) * 8.0, c12 = (double)((t12 + s12 - 1) / s12) * 12.0 / 1.06;
+  return c12 < c8 ? dq_v<64, 12>(a) : dq_v<64, 8>(a);
+}
+
 hipError_t launch_bwd_dq(const BwdArgs& a) {
   if (a.ds != nullptr) return launch_bwd_dq_ds(a);
   switch (tile_width(a.d)) {
-    case 64: return dq_v<64, 8>(a);
+    case 64: return dq_64(a);
     case 96: return dq_v<96, 8>(a);
     case 128: return dq_v<128, 8>(a);
     default: return dq_v<160, 8>(a);
