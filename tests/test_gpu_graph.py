@@ -119,3 +119,50 @@ def test_first_backward_call_inside_capture():
                        timeout=300)
     print(r.stdout[-2000:], r.stderr[-2000:], flush=True)
     assert r.returncode == 0 and "first captured call ok" in r.stdout
+
+
+_NOALLOC_CAPTURED = r"""
+import sys
+import numpy as np
+import torch
+sys.path.insert(0, sys.argv[1])
+sys.path.insert(0, sys.argv[1] + "/tests")
+import paper_2405_15780_amd as va
+import workloads
+from gpu_util import to_device
+B, H, N, d = 1, 6, 2300, 64
+x = {n: to_device(a) for n, a in workloads.make_small_inputs(B, H, N, d, seed=6500).items()}
+f32 = dict(dtype=torch.float32, device="cuda")
+o, lse = torch.empty((B, H, N, d), **f32), torch.empty((B, H, N), **f32)
+grads = tuple(torch.empty((B, H, N, d), **f32) for _ in range(3))
+torch.cuda.synchronize()
+g = torch.cuda.CUDAGraph()
+with torch.cuda.graph(g):  # the process's first forward and backward calls, without a workspace
+    va.fwd(x["q"], x["k"], x["v"], out=(o, lse))
+    va.bwd_noalloc(x["q"], x["k"], x["v"], o, lse, x["dout"], out=grads)
+for rep in range(3):
+    g.replay()
+    torch.cuda.synchronize()
+    o2, lse2 = va.fwd(x["q"], x["k"], x["v"])
+    ref = va.bwd(x["q"], x["k"], x["v"], o2, lse2, x["dout"])
+    torch.cuda.synchronize()
+    for name, a, b in zip(("o", "lse", "dq", "dk", "dv"), (o, lse) + grads, (o2, lse2) + ref):
+        assert torch.equal(a, b), (rep, name)
+print("captured noalloc step ok", flush=True)
+"""
+
+
+def test_first_calls_captured_with_the_allocation_free_backward():
+    # A fresh process whose first forward and backward calls are captured:
+    # the once-per-device lookups (resident workgroups of the d <= 64 kernel
+    # variants, the static scratch's device address) happen during capture,
+    # and the allocation-free backward needs no workspace there.
+    import os
+    import subprocess
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    print("case first calls inside capture with bwd_noalloc (child process)", flush=True)
+    r = subprocess.run([sys.executable, "-c", _NOALLOC_CAPTURED, root], capture_output=True, text=True, timeout=300)
+    print(r.stdout[-2000:], r.stderr[-2000:], flush=True)
+    assert r.returncode == 0 and "captured noalloc step ok" in r.stdout
