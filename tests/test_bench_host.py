@@ -27,3 +27,31 @@ def test_kernel_source_digests_are_per_family():
     d = {row: bench.kernel_sources_digest(row) for row in bench.KERNEL_FILES}
     assert d["attention"] == d["d72"] == d["d160"] == d["bnhd"] == d["d64"] == d["m1"]
     assert len({d["attention"], d["merge"], d["ulysses"], d["agg"]}) == 4
+
+
+def test_default_backward_is_the_recompute_mode():
+    sys.path.insert(0, ROOT)
+    import bench
+
+    old = sys.argv
+    try:
+        sys.argv = ["bench.py"]
+        assert bench.parse().bwd_mode == "recompute"
+    finally:
+        sys.argv = old
+
+
+def test_cpu_baseline_walks_the_workload_and_repeats_a_small_one():
+    import types
+
+    sys.path.insert(0, ROOT)
+    import bench
+    import workloads
+
+    for backward in (True, False):
+        w = types.SimpleNamespace(B=1, H=2, N=300, d=16, scale=0.25, backward=backward)
+        x = workloads.make_small_inputs(1, 2, 300, 16, seed=3)
+        r = bench.cpu_baseline(w, x, 0.2)
+        assert r["kind"] == "oracle" and r["unit"] == "TFLOP/s" and r["value"] > 0 and r["cores"] >= 1
+        assert "times over" in r["sample"]  # 600 rows take far less than the budget
+        assert ("forward+backward" in r["sample"]) == backward
