@@ -3,17 +3,22 @@
 // the saved logsumexp, never stored.
 //
 //   1. preprocess:  D_i = sum_c dO_ic O_ic                (HBM-bound)
-//   2. dK/dV kernel: one workgroup per 128 keys (32 per wave, K and V held in
-//      registers); streams Q, dO, LSE and D in tiles of 64 queries:
+//   2. dK/dV kernel: one workgroup per 128 keys (192 at head dims up to 64;
+//      32 per wave, K and V held in registers); streams Q, dO, LSE and D in
+//      tiles of 64 queries:
 //        S = Q K^T, P = exp2(S*scale*log2e - LSE*log2e)
 //        dV^T += dO^T P,  dP = dO V^T,  dS = P o (dP - D),  dK^T += Q^T dS
-//   3. dQ kernel: one workgroup per 128 queries (32 per wave, Q and dO held in
-//      registers); streams K and V in tiles of 64 keys:
+//   3. dQ kernel: one workgroup per 256 queries (or 384 at head dims up to 64;
+//      32 per wave, Q and dO held in registers); streams K and V in tiles of
+//      32 keys:
 //        S^T = K Q^T, P^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T
 // Splitting dQ from dK/dV costs one extra recomputation of S and dP but needs
-// no atomics for dQ. The only atomics are those of the dK/dV kernel's split
-// key blocks (two fp32 adds onto zero per element, which commute exactly), so
-// results are deterministic. As in the forward pass, operands
+// no atomics for dQ (accumulating dQ inside the dK/dV pass would add a 4-byte
+// atomic per query, key block and column, B H N^2 d / 32 of them, and fp32
+// atomics sustain only ~1.3 TB/s on this part). The only atomics are those of
+// the dK/dV kernel's split key blocks (two fp32 adds onto zero per element,
+// which commute exactly, and every whole block forms the same two rounded
+// partial sums), so results are deterministic and independent of the grid. As in the forward pass, operands
 // may have any batch / head / row strides, and a head dim d below the tile
 // width D is padded with zero columns on load and cut off on store.
 #include <atomic>
@@ -23,9 +28,6 @@
 #include "vitattn_launch.h"
 
 namespace vitattn {
-
-constexpr int kBwdWaves = 4;
-constexpr int kBwdThreads = 64 * kBwdWaves;
 
 // ------------------------------------------------------------------ preprocess
 
@@ -63,7 +65,6 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __
 
 // ------------------------------------------------------------------ dK / dV
 
-constexpr int kDkvBK = 32 * kBwdWaves;  // keys per workgroup (KBW = kBwdWaves key blocks)
 constexpr int kDkvBQ = 64;              // queries per streamed tile
 constexpr int kDkvAhead = 2;            // LDS operand reads this many matrix-core ops ahead (3 measured no better)
 
