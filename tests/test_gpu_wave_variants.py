@@ -45,3 +45,32 @@ def test_twelve_wave_grid_matches_single_heads_and_oracle(d):
     kk = t.from_numpy(keys).cuda()
     assert_close({"dk": np64(full["dk"][0, h][kk]), "dv": np64(full["dv"][0, h][kk])}, {"dk": dk, "dv": dv},
                  names=("dk", "dv"), label=f"wave variants d={d} sampled key rows")
+
+
+def test_twelve_wave_grid_in_the_sequence_major_layout():
+    # the same grid through the strided entry points ([B, N, H, d] operands
+    # and outputs, as an all-to-all hands them over): bitwise equal to the
+    # dense call, which takes the same kernel variants
+    import paper_2405_15780_amd as va
+
+    t = torch()
+    B, H, N, d = 1, 6, 22001, 64
+    print(f"case wave variants sequence-major B={B} H={H} N={N} d={d}", flush=True)
+    x = workloads.make_small_inputs(B, H, N, d, seed=9990)
+    scale = 1.0 / np.sqrt(d)
+    dense = run_hip(x, scale)
+
+    def bnhd(bits):  # stored [B, N, H, d], viewed as [B, H, N, d]
+        a = t.from_numpy(np.ascontiguousarray(bits.transpose(0, 2, 1, 3)).view(np.int16)).view(t.bfloat16).cuda()
+        return a.transpose(1, 2)
+
+    dev = {n: bnhd(a) for n, a in x.items()}
+    f32 = dict(dtype=t.float32, device="cuda")
+    outs = [t.empty((B, N, H, d), **f32).transpose(1, 2) for _ in range(4)]
+    o, dq, dk, dv = outs
+    lse = t.empty((B, H, N), **f32)
+    va.fwd(dev["q"], dev["k"], dev["v"], scale, out=(o, lse))
+    va.bwd(dev["q"], dev["k"], dev["v"], o, lse, dev["dout"], scale, out=(dq, dk, dv))
+    t.cuda.synchronize()
+    for name, a in (("o", o), ("lse", lse), ("dq", dq), ("dk", dk), ("dv", dv)):
+        assert t.equal(a, dense[name]), name
