@@ -72,6 +72,38 @@ def oracle_all_heads(x, scale):
     return out
 
 
+def oracle_one_head(x, scale, b, h, block=256):
+    """All outputs of head (b, h) from the oracle, its query blocks evaluated
+    concurrently (oracle.forward_backward_rows on a thread pool, BLAS held to
+    one thread per task) and the blocks' dK, dV contributions summed in block
+    order: the oracle's arithmetic, with a head too long for one core done in
+    parallel."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+
+    N = x["q"].shape[2]
+    starts = list(range(0, N, block))
+
+    def one(r0):
+        return oracle.forward_backward_rows(x["q"], x["k"], x["v"], x["dout"], scale, b, h, r0, min(N, r0 + block))
+
+    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    d = x["q"].shape[3]
+    out = {"o": np.empty((N, d)), "lse": np.empty(N), "dq": np.empty((N, d)), "dk": np.zeros((N, d)),
+           "dv": np.zeros((N, d))}
+    with threadpool_limits(1), ThreadPoolExecutor(workers) as ex:
+        for r0, r in zip(starts, ex.map(one, starts)):
+            r1 = min(N, r0 + block)
+            out["o"][r0:r1], out["lse"][r0:r1], out["dq"][r0:r1] = r["o"], r["lse"], r["dq"]
+            out["dk"] += r["dk_part"]
+            out["dv"] += r["dv_part"]
+    return out
+
+
 def rel_l2(got, ref):
     return float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
 

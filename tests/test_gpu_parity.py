@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import workloads
-from gpu_util import assert_close, oracle_all_heads, run_hip, to_device, torch
+from gpu_util import assert_close, oracle_all_heads, oracle_one_head, run_hip, to_device, torch
 
 pytestmark = pytest.mark.gpu
 
@@ -136,6 +136,34 @@ def test_long_sequence_workloads_sampled(cid, store_ds):
     assert_close(got, {"dk": gold["dk"].astype(np.float64), "dv": gold["dv"].astype(np.float64)},
                  names=("dk", "dv"), label=f"{w.name} sampled key rows")
     _identities(w, x, res)
+
+
+def test_ulysses_shard_N65536_one_head_full_compare():
+    """One whole head (b=0, h=1) of the 65,536-token d=128 workload compared
+    element by element in all five outputs: every key row's dK and dV at full
+    size, beyond the sampled rows of the test above."""
+    w = workloads.WORKLOADS[3]
+    x = workloads.make_inputs(w)
+    res = run_hip(x, w.scale)
+    print(f"{w.name}: fp64 oracle of head (0, 1) over its 65,536 query rows", flush=True)
+    ref = oracle_one_head(x, w.scale, 0, 1)
+    got = {n: np64(t[0, 1]) for n, t in res.items()}
+    assert_close(got, ref, label=f"{w.name} head (0,1) in full")
+
+
+def test_paper_scale_N188416_one_head_full_compare():
+    """One whole head (b=0, h=0) of the paper-scale 188,416-token d=128
+    workload (the benchmark's) compared element by element in all five
+    outputs against the fp64 oracle."""
+    w = workloads.WORKLOADS[4]
+    x = workloads.make_inputs(w)
+    res = run_hip(x, w.scale)
+    got = {n: np64(t[0, 0]) for n, t in res.items()}
+    del res
+    torch().cuda.empty_cache()
+    print(f"{w.name}: fp64 oracle of head (0, 0) over its 188,416 query rows", flush=True)
+    ref = oracle_one_head(x, w.scale, 0, 0, block=128)
+    assert_close(got, ref, label=f"{w.name} head (0,0) in full")
 
 
 def test_one_million_tokens_sampled():
