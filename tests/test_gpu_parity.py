@@ -120,7 +120,7 @@ def test_vit_block_N16384_x8_head_all_heads_full_compare(store_ds):
 def test_long_sequence_workloads_sampled(cid, store_ds):
     """The 65,536-token (H=4, d=128) and 188,416-token (H=2, d=128) workloads
     at full size in both backward modes (the benchmark times the 188,416-token
-    one with the dS mode when its workspace fits)."""
+    one with the recompute backward and the opt-in dS mode beside it)."""
     w = workloads.WORKLOADS[cid]
     print(f"{w.name} ({'stored-ds' if store_ds else 'recompute'} backward): generating inputs", flush=True)
     x = workloads.make_inputs(w)
