@@ -257,8 +257,12 @@ class SmiSampler:
             return None
         import statistics
 
-        # drop readings taken while the GPU was still idle or ramping
-        busy = [(p, c) for p, c in self.samples if c >= 500.0] or self.samples
+        # drop readings taken while the GPU was still idle or ramping; a timed
+        # region shorter than amd-smi's sampling interval may have none left,
+        # and then nothing is reported
+        busy = [(p, c) for p, c in self.samples if c >= 500.0]
+        if not busy:
+            return None
         pw = [p for p, _ in busy]
         clk = [c for _, c in busy]
         return {"samples": len(busy), "power_w_median": statistics.median(pw),

@@ -1,6 +1,8 @@
 """Host-side behaviour of bench.py that needs no GPU: more than one GPU is
 refused with a JSON message (and exit status 2) before anything touches a
-device, for the default workload and the other rows."""
+device, for the default workload and the other rows; and the host logic around
+the measurement (source digests, defaults, the CPU baseline's sampling, the
+clock summary)."""
 import json
 import os
 import subprocess
@@ -56,3 +58,17 @@ def test_cpu_baseline_walks_the_workload_and_repeats_a_small_one():
         assert r["kind"] == "oracle" and r["unit"] == "TFLOP/s" and r["value"] > 0 and r["cores"] >= 1
         assert "times over" in r["sample"], r["sample"]  # 128 tiny rows take far less than the budget
         assert ("forward+backward" in r["sample"]) == backward
+
+
+def test_clock_summary_ignores_idle_samples():
+    # readings below 500 MHz are the GPU idle or ramping; a timed region too
+    # short to catch the GPU busy reports no clock rather than idle readings
+    sys.path.insert(0, ROOT)
+    import bench
+
+    s = bench.SmiSampler()
+    s.samples = [(253.0, 157.0), (252.0, 158.0)]
+    assert s.summary() is None
+    s.samples = [(253.0, 157.0), (1300.0, 1900.0), (1320.0, 2000.0)]
+    got = s.summary()
+    assert got["samples"] == 2 and got["sclk_mhz_min"] == 1900.0 and got["power_w_median"] == 1310.0
