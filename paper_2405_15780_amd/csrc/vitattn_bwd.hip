@@ -3,9 +3,9 @@
 // the saved logsumexp, never stored.
 //
 //   1. preprocess:  D_i = sum_c dO_ic O_ic                (HBM-bound)
-//   2. dK/dV kernel: one workgroup per 128 keys (192 at head dims up to 64;
-//      32 per wave, K and V held in registers); streams Q, dO, LSE and D in
-//      tiles of 64 queries:
+//   2. dK/dV kernel: one workgroup per 128 keys (256 at head dims up to 64;
+//      32 or 64 per wave, K and V held in registers); streams Q, dO, LSE and
+//      D in tiles of 64 queries:
 //        S = Q K^T, P = exp2(S*scale*log2e - LSE*log2e)
 //        dV^T += dO^T P,  dP = dO V^T,  dS = P o (dP - D),  dK^T += Q^T dS
 //   3. dQ kernel: one workgroup per 256 queries (or 384 at head dims up to 64;
@@ -77,15 +77,21 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_void_t*)(lds_stats + kDkvBQ), 4, (row0 + lane) * 4, 0, 0, 0);
 }
 
-// One workgroup = 2*KBW waves = 32*KBW keys of one (b, h), in KBW blocks of
-// 32 keys (KBW = 4: 8 waves, 128 keys; 6 at the narrowest tile: 12 waves).
-// Each key block has two waves with split roles (waves share the SIMDs round
-// robin, so the vector and matrix phases of the roles interleave):
+// One workgroup = 2*KBW waves = 32*KBW*KPW keys of one (b, h): KBW pairs of
+// waves, each pair owning KPW blocks of 32 keys (KBW = 4, KPW = 1: 8 waves,
+// 128 keys; KBW = 4, KPW = 2 at the narrowest tile: 8 waves, 256 keys). The
+// two waves of a pair split the roles (waves share the SIMDs round robin, so
+// the vector and matrix phases of the roles interleave):
 //   role P  (waves 0 .. KBW-1): holds K, accumulates dV^T.
 //     S = Q K^T;  P = exp2(S*scale*log2e - LSE2);  dV^T += dO^T P;
 //     writes P (bf16) to LDS for its partner.
 //   role dS (waves KBW .. 2*KBW-1): holds V, accumulates dK^T, one tile behind.
 //     dP = dO V^T;  dS = P o (dP - D) with the partner's P;  dK^T += Q^T dS.
+// A wave with KPW key blocks reads each streamed operand from LDS once and
+// feeds it to the matrix-core op of every block, and reads the row
+// statistics once for all of them, so these LDS reads per matrix-core op
+// shrink by a factor KPW (the P exchange stays per key block). Each key
+// block's ops, and so its bits, are the same for every KPW.
 // Q, dO and the row statistics stream through a ring of three LDS slots in
 // tiles of 64 queries (two blocks of 32); in iteration t role P works on
 // tile t and role dS on tile t-1, and tile t+1 is being fetched. Query rows
@@ -95,8 +101,9 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 // slot index is then a compile-time constant (LDS addresses fold into
 // instruction immediates).
 //
-// Each wave's work per tile is one stream of 4*D/16 matrix-core ops whose
-// LDS operands are read two ops ahead, in four phases (query blocks 0, 1):
+// Each wave's work per tile is one stream of 4*KPW*D/16 matrix-core ops whose
+// LDS operands are read two operands ahead, in four phases (query blocks 0,
+// 1; within a phase the KPW ops that share an operand are adjacent):
 //   1. first product of block 0 (S or dP)
 //   2. first product of block 1;  vector units: P or dS of block 0
 //   3. second product of block 0 (dV or dK);  vector units: block 1
@@ -114,7 +121,7 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 // own a key block and every query; the key blocks after them (at most half a
 // round of them) are split into two workgroups each, one per half of the
 // query tiles, which add their dK and dV into rows the launch zeroed first.
-template <int D, bool STORE_DS, int KBW>
+template <int D, bool STORE_DS, int KBW, int KPW>
 __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per_eu(KBW / 2, KBW / 2))) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
@@ -122,13 +129,15 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
     const Map mv, const Map mg, const Map mdk, const Map mdv, int H, int dr, int Nq, int Nk, int n_ktiles,
     int n_whole, float c, float scale) {
   constexpr int KK = D / 16, NCB = D / 32;
-  constexpr int PH = KK;           // ops per phase
-  constexpr int NOPS = 4 * PH;     // ops per tile
+  constexpr int PH = KK;           // operands per phase (each feeding KPW ops)
+  constexpr int NA = 4 * PH;       // streamed operands per tile
   // query rows of vector work: row r rides on op slot r * PH / 16 of its phase
   constexpr int TILE_BYTES = kDkvBQ * D * 2;
   constexpr int RING = 3;
   constexpr int NWAVES = 2 * KBW;
-  constexpr int BK = 32 * KBW;  // keys per workgroup
+  constexpr int BK = 32 * KBW * KPW;  // keys per workgroup
+  static_assert(KPW == 1 || !STORE_DS, "stored dS blocks are laid out per wave of one key block");
+  static_assert(KPW == 1 || D != 160, "the widest tile has no registers for a second key block");
   // One variable per ring slot: the compiler then knows that reading one
   // slot never overlaps the DMA into another and inserts no wait for it.
   __shared__ __attribute__((aligned(1024))) char qbuf0[TILE_BYTES];
@@ -144,13 +153,13 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
   char* const qbuf[RING] = {qbuf0, qbuf1, qbuf2};
   char* const gbuf[RING] = {gbuf0, gbuf1, gbuf2};
   float* const sbuf[RING] = {sbuf0, sbuf1, sbuf2};
-  // P exchange: [slot][key block][query block][contraction step][lane] of 8
-  // bf16. Role P writes tile t's P at the end of iteration t and role dS reads
+  // P exchange: [slot][wave pair][key block of the pair][query block]
+  // [contraction step][lane] of 8 bf16. Role P writes tile t's P at the end of iteration t and role dS reads
   // it at the start of iteration t+1, so two slots (by tile parity) suffice;
   // the narrower tiles use the ring slot instead, a compile-time index. The
   // widest tile needs the two-slot form to fit in LDS.
   constexpr int XR = D == 160 ? 2 : RING;
-  __shared__ __attribute__((aligned(16))) uint4 xbuf[XR][KBW][2][2][64];
+  __shared__ __attribute__((aligned(16))) uint4 xbuf[XR][KBW][KPW][2][2][64];
   debug_poison_lds(qbuf0, qbuf1, qbuf2, gbuf0, gbuf1, gbuf2, sbuf0, sbuf1, sbuf2, xbuf);
 
   // this workgroup's key block (work item) and query tiles [t0, t1)
@@ -195,14 +204,18 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
   rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)qend * 4);
   rsrc_t rl = make_rsrc(lse2 + (size_t)bh * Nq, (unsigned)qend * 4);
 
-  // held fragments (B operands, columns = this block's keys): K for role P, V for role dS
-  const int key = kt * BK + kb * 32 + (lane & 31);
+  // held fragments (B operands, columns = this block's keys): K for role P,
+  // V for role dS; this lane's key in block kp is key0 + 32 kp
+  const int key0 = kt * BK + kb * 32 * KPW + (lane & 31);
   const Map& mh = role_p ? mk : mv;
   const int ldh = 2 * mh.ld;
   const rsrc_t rh = make_rsrc((role_p ? k : v) + mh.head(bh, H), (unsigned)(Nk * ldh));
-  bf16x8 hf[KK];
+  bf16x8 hf[KPW][KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) hf[kk] = as_bf16x8(buffer_load16(rh, chunk_offset(key, 2 * kk + h, ldh, chr)));
+  for (int kp = 0; kp < KPW; ++kp)
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      hf[kp][kk] = as_bf16x8(buffer_load16(rh, chunk_offset(key0 + 32 * kp, 2 * kk + h, ldh, chr)));
 
   // Q and dO tiles. With STORE_DS only the four role-P waves fetch tiles, so
   // the dS waves never wait for a DMA request (and with it, for their stores).
@@ -216,34 +229,40 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
   tf.init(lane);
   constexpr int DMA_PER_TILE = 2 * decltype(dma)::PER_WAVE + 2;  // loads per wave per tile
 
-  f32x16 acc[NCB];  // dV^T (role P) or dK^T (role dS)
+  f32x16 acc[KPW][NCB];  // dV^T (role P) or dK^T (role dS) per key block
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero16();
+  for (int kp = 0; kp < KPW; ++kp)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) acc[kp][cb] = zero16();
 
-  // Output row of this lane's key (dV for role P, dK for role dS) and the
-  // factor of its accumulator.
-  auto out_row = [&]() -> float* {
+  // Output row of this lane's key in block kp (dV for role P, dK for role
+  // dS) and the factor of its accumulator.
+  auto out_row = [&](int kp) -> float* {
     const Map& mout = role_p ? mdv : mdk;
-    return (role_p ? dv : dk) + mout.head(bh, H) + (size_t)key * mout.ld;
+    return (role_p ? dv : dk) + mout.head(bh, H) + (size_t)(key0 + 32 * kp) * mout.ld;
   };
   const float f = role_p ? 1.f : scale;
   // Whole blocks, after their last tile below mid: store the first partial
   // (rounded like the split halves' addends) and restart the sum.
   auto store_first_part = [&]() __attribute__((always_inline)) {
-    if (key < Nk) {
-      float* out = out_row();
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
+    for (int kp = 0; kp < KPW; ++kp) {
+      if (key0 + 32 * kp < Nk) {
+        float* out = out_row(kp);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int col = 32 * cb + 8 * g + 4 * h;
-          if (col < dr)
-            *reinterpret_cast<float4*>(out + col) = make_float4(acc[cb][4 * g] * f, acc[cb][4 * g + 1] * f,
-                                                                acc[cb][4 * g + 2] * f, acc[cb][4 * g + 3] * f);
-        }
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int col = 32 * cb + 8 * g + 4 * h;
+            if (col < dr)
+              *reinterpret_cast<float4*>(out + col) =
+                  make_float4(acc[kp][cb][4 * g] * f, acc[kp][cb][4 * g + 1] * f, acc[kp][cb][4 * g + 2] * f,
+                              acc[kp][cb][4 * g + 3] * f);
+          }
+      }
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) acc[kp][cb] = zero16();
     }
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero16();
   };
 
   // Tiles are numbered from t0 in the loops below. STORE_DS: the dS operands
@@ -279,27 +298,28 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
   // One tile of one role, in ring slot SL. Role P: S/P/dV; role dS: dP/dS/dK.
   // The row statistics (and role dS's P) of both query blocks are read
   // before `prefetch` requests the next tile, so that none of these LDS
-  // reads has to wait for that DMA. The widest tile has no registers to
-  // spare for both blocks: there block 1's are read into block 0's
-  // registers once block 0's vector work is done (end of phase 2).
+  // reads has to wait for that DMA. The widest tile, and waves with more than
+  // one key block, have no registers to spare for both blocks: there block
+  // 1's are read into block 0's registers once block 0's vector work is done
+  // (end of phase 2).
   auto run_tile = [&](auto role_tag, auto slot_tag, int tile, auto&& prefetch) {
     constexpr bool RP = decltype(role_tag)::value;
     constexpr int SL = decltype(slot_tag)::value;
     const char* qs = qbuf[SL];
     const char* gs = gbuf[SL];
     const float* st = sbuf[SL];
-    uint4(*xb)[2][64] = xbuf[XR == RING ? SL : (tile & 1)][kb];
+    uint4(*xb)[2][2][64] = xbuf[XR == RING ? SL : (tile & 1)][kb];  // [key block][query block][step][lane]
 
-    f32x16 m1[2];          // S (P) or dP (dS), per query block
-    bf16x8 ob[2][2];       // bf16 operands of P or dS [block][contraction step]
-    constexpr bool LEAN = D == 160;
+    f32x16 m1[KPW][2];     // S (P) or dP (dS), per key block and query block
+    bf16x8 ob[KPW][2][2];  // bf16 operands of P or dS [key block][query block][contraction step]
+    constexpr bool LEAN = D == 160 || KPW > 1;
     constexpr int NSB = LEAN ? 1 : 2;  // query blocks whose side data is held at once
     float4 stat[NSB][4];   // LSE2 (role P) or D (role dS) of the block's rows
-    uint4 pin4[NSB][2];    // role dS: the partner's P, as bf16 pairs
+    uint4 pin4[KPW][NSB][2];  // role dS: the partner's P, as bf16 pairs
 
-    // A operand of op i
-    auto read_a = [&](int i) -> bf16x8 {
-      const int ph = i / PH, j = i % PH, qb = ph & 1;
+    // streamed operand a (shared by the KPW ops of one phase slot)
+    auto read_a = [&](int a) -> bf16x8 {
+      const int ph = a / PH, j = a % PH, qb = ph & 1;
       if (ph < 2) return lds_frag_row(RP ? qs : gs, qb * 32 * 2 * D + rf.at(j));
       return tf.load(RP ? gs : qs, qb * 32 + 16 * (j / NCB), j % NCB);
     };
@@ -309,11 +329,14 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
       for (int g = 0; g < 4; ++g)
         stat[sb][g] = *reinterpret_cast<const float4*>(st + (RP ? kDkvBQ : 0) + qb * 32 + 8 * g + 4 * h);
       if constexpr (!RP) {
-        pin4[sb][0] = xb[qb][0][lane];
-        pin4[sb][1] = xb[qb][1][lane];
+#pragma unroll
+        for (int kp = 0; kp < KPW; ++kp) {
+          pin4[kp][sb][0] = xb[kp][qb][0][lane];
+          pin4[kp][sb][1] = xb[kp][qb][1][lane];
+        }
       }
     };
-    auto valu = [&](int qb, int u) {
+    auto valu = [&](int kp, int qb, int u) {
       // rows u*16/PH .. (u+1)*16/PH - 1 (PH = 4 or 8: 16/PH rows per slot)
       constexpr int RMAX = (16 + PH - 1) / PH;
 #pragma unroll
@@ -324,56 +347,59 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
         const float sv = stat[sb][r >> 2][r & 3];
         float x;
         if constexpr (RP) {
-          x = __builtin_amdgcn_exp2f(__builtin_fmaf(m1[qb][r], c, -sv));
+          x = __builtin_amdgcn_exp2f(__builtin_fmaf(m1[kp][qb][r], c, -sv));
         } else {
-          const unsigned w = pin4[sb][r >> 3][(r & 7) >> 1];
+          const unsigned w = pin4[kp][sb][r >> 3][(r & 7) >> 1];
           const float p = __uint_as_float((r & 1) ? (w & 0xffff0000u) : (w << 16));
-          x = p * (m1[qb][r] - sv);
+          x = p * (m1[kp][qb][r] - sv);
         }
         pin(x);
-        m1[qb][r] = x;
-        if ((r & 7) == 7) ob[qb][r >> 3] = acc_to_operand(m1[qb], r >> 3);
+        m1[kp][qb][r] = x;
+        if ((r & 7) == 7) ob[kp][qb][r >> 3] = acc_to_operand(m1[kp][qb], r >> 3);
       }
     };
 
     if constexpr (!RP) flush_ds();  // the previous tile's dS, before this tile's DMA requests
     read_side(0);
     if constexpr (!LEAN) read_side(1);
-    constexpr int AH = kDkvAhead;  // operand reads run AH ops ahead of their matrix-core op
+    constexpr int AH = kDkvAhead;  // operand reads run AH operands ahead of their matrix-core ops
     bf16x8 aq[AH + 1];
 #pragma unroll
-    for (int i = 0; i < AH; ++i) aq[i] = read_a(i);
+    for (int a = 0; a < AH; ++a) aq[a] = read_a(a);
     sched_fence();
     prefetch();
     sched_fence();
     // every op index a compile-time constant (the widest tile's stream is too
     // long for the unroller's size limit, and register arrays indexed at run
     // time would live in scratch memory)
-    static_for<0, NOPS>([&](auto IC) __attribute__((always_inline)) {
+    static_for<0, NA * KPW>([&](auto IC) __attribute__((always_inline)) {
       constexpr int i = decltype(IC)::value;
-      constexpr int ph = i / PH, j = i % PH, qb = ph & 1;
-      if constexpr (i + AH < NOPS) aq[(i + AH) % (AH + 1)] = read_a(i + AH);
+      constexpr int a = i / KPW, kp = i % KPW;  // operand, key block
+      constexpr int ph = a / PH, j = a % PH, qb = ph & 1;
+      if constexpr (kp == 0 && a + AH < NA) aq[(a + AH) % (AH + 1)] = read_a(a + AH);
       if constexpr (ph < 2) {
-        if constexpr (j == 0) m1[qb] = zero16();
-        m1[qb] = mfma32(aq[i % (AH + 1)], hf[j], m1[qb]);
-        if constexpr (ph == 1) valu(0, j);
-        if constexpr (LEAN && i == 2 * PH - 1) read_side(1);
+        if constexpr (j == 0) m1[kp][qb] = zero16();
+        m1[kp][qb] = mfma32(aq[a % (AH + 1)], hf[kp][j], m1[kp][qb]);
+        if constexpr (ph == 1) valu(kp, 0, j);
+        if constexpr (LEAN && i == 2 * PH * KPW - 1) read_side(1);
       } else {
-        acc[j % NCB] = mfma32(aq[i % (AH + 1)], ob[qb][j / NCB], acc[j % NCB]);
-        if constexpr (ph == 2) valu(1, j);
+        acc[kp][j % NCB] = mfma32(aq[a % (AH + 1)], ob[kp][qb][j / NCB], acc[kp][j % NCB]);
+        if constexpr (ph == 2) valu(kp, 1, j);
       }
       sched_fence();
     });
     if constexpr (RP) {
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
+      for (int kp = 0; kp < KPW; ++kp)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) xb[qb][ks][lane] = __builtin_bit_cast(uint4, ob[qb][ks]);
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) xb[kp][qb][ks][lane] = __builtin_bit_cast(uint4, ob[kp][qb][ks]);
     } else if constexpr (STORE_DS) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) pend[qb][ks] = ob[qb][ks];
+        for (int ks = 0; ks < 2; ++ks) pend[qb][ks] = ob[0][qb][ks];
       pend_tile = tile;
     }
   };
@@ -499,9 +525,11 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
   }
   (void)DMA_PER_TILE;
 
-  if (key < Nk) {
-    float* out = out_row();
-    if (two_part) wait_vmem();  // the first partial's stores have completed
+  if (two_part) wait_vmem();  // the first partial's stores have completed
+#pragma unroll
+  for (int kp = 0; kp < KPW; ++kp) {
+    if (key0 + 32 * kp >= Nk) continue;
+    float* out = out_row(kp);
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
@@ -511,7 +539,7 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
           float x[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            x[e] = acc[cb][4 * g + e] * f;
+            x[e] = acc[kp][cb][4 * g + e] * f;
             pin(x[e]);  // rounded product, never fused into the add below
           }
           if (split) {
@@ -963,7 +991,7 @@ static hipError_t rowdot_l(const BwdArgs& a) {
 
 // Workgroups of the dK/dV kernel resident on the current device at once
 // (0 if the runtime cannot say), looked up once per device.
-template <int D, bool STORE_DS, int KBW>
+template <int D, bool STORE_DS, int KBW, int KPW>
 static int dkdv_resident_workgroups() {
   static std::atomic<int> known[64];  // per device ordinal; 0 = not looked up, -1 = unknown
   int dev = 0;
@@ -972,8 +1000,8 @@ static int dkdv_resident_workgroups() {
   if (n == 0) {
     int per_cu = 0, cus = 0;
     n = -1;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dkdv_kernel<D, STORE_DS, KBW>, 128 * KBW,
-                                                     0) == hipSuccess &&
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dkdv_kernel<D, STORE_DS, KBW, KPW>,
+                                                     128 * KBW, 0) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && per_cu * cus > 0)
       n = per_cu * cus;
     known[dev].store(n, std::memory_order_relaxed);
@@ -981,14 +1009,14 @@ static int dkdv_resident_workgroups() {
   return n > 0 ? n : 0;
 }
 
-template <int D, bool STORE_DS, int KBW>
+template <int D, bool STORE_DS, int KBW, int KPW>
 static hipError_t dkdv_s(const BwdArgs& a) {
-  constexpr int BK = 32 * KBW;
+  constexpr int BK = 32 * KBW * KPW;
   const int n_kt = (a.Nk + BK - 1) / BK;
   const int total = a.BH * n_kt;
   // A last round at most half full is split in two halves of the query range
   // (when there are two query tiles to split), so that it takes half as long.
-  const int slots = dkdv_resident_workgroups<D, STORE_DS, KBW>();
+  const int slots = dkdv_resident_workgroups<D, STORE_DS, KBW, KPW>();
   const int tail = slots > 0 ? total % slots : 0;
   int n_whole = total;
   if (tail > 0 && 2 * tail <= slots && (a.Nq + kDkvBQ - 1) / kDkvBQ >= 2) {
@@ -997,36 +1025,40 @@ static hipError_t dkdv_s(const BwdArgs& a) {
                        a.d, a.Nk, n_kt, n_whole, BK);
   }
   const int grid = n_whole + 2 * (total - n_whole);
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS, KBW>), dim3(grid), dim3(64 * 2 * KBW), 0, a.stream, a.q,
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS, KBW, KPW>), dim3(grid), dim3(64 * 2 * KBW), 0, a.stream, a.q,
                      a.k, a.v, a.dout, a.drow, a.lse2, a.dk, a.dv, a.ds, a.mq, a.mk, a.mv, a.mg, a.mdk, a.mdv, a.H,
                      a.d, a.Nq, a.Nk, n_kt, n_whole, a.scale * kLog2e, a.scale);
   return hipGetLastError();
 }
-// Key blocks of 32 per workgroup (two waves each): four, except at the
-// narrowest tile in the recompute mode, whose 166 VGPRs leave room for three
-// waves per SIMD: six key blocks (12 waves, 192 keys) stream each Q / dO tile
-// to half again as many keys. The dS mode keeps four (its stored dS blocks are
-// laid out per 128 keys).
+// Four pairs of waves per workgroup. At the narrowest tile in the recompute
+// mode each wave holds two 32-key blocks (234 VGPRs, two waves per SIMD, 256
+// keys per workgroup), so every operand it reads from LDS feeds two
+// matrix-core ops and every Q / dO tile it streams serves twice the keys:
+// 8 % faster than six one-block pairs at three waves per SIMD (B=4, H=1,
+// N=188,416, d=64), with the same bits. At the wider tiles two blocks per
+// wave leave room for one wave per SIMD only, which measured 5 % slower at
+// d=128 and no faster at d=96. The dS mode keeps one block per wave (its
+// stored dS blocks are laid out per 128 keys).
 template <int D>
 static hipError_t dkdv_d(const BwdArgs& a) {
-  if (a.ds != nullptr) return dkdv_s<D, true, 4>(a);
-  return dkdv_s<D, false, D == 64 ? 6 : 4>(a);
+  if (a.ds != nullptr) return dkdv_s<D, true, 4, 1>(a);
+  return dkdv_s<D, false, 4, D == 64 ? 2 : 1>(a);
 }
 
-#define VITATTN_DKDV_INSTANTIATE(D, S, KBW)                                                                    \
-  template __global__ void attn_bwd_dkdv_kernel<D, S, KBW>(                                                   \
+#define VITATTN_DKDV_INSTANTIATE(D, S, KBW, KPW)                                                               \
+  template __global__ void attn_bwd_dkdv_kernel<D, S, KBW, KPW>(                                              \
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
       float* __restrict__, uint16_t* __restrict__, const Map, const Map, const Map, const Map, const Map,      \
       const Map, int, int, int, int, int, int, float, float);
-VITATTN_DKDV_INSTANTIATE(128, false, 4)
-VITATTN_DKDV_INSTANTIATE(64, false, 6)
-VITATTN_DKDV_INSTANTIATE(96, false, 4)
-VITATTN_DKDV_INSTANTIATE(160, false, 4)
-VITATTN_DKDV_INSTANTIATE(128, true, 4)
-VITATTN_DKDV_INSTANTIATE(64, true, 4)
-VITATTN_DKDV_INSTANTIATE(96, true, 4)
-VITATTN_DKDV_INSTANTIATE(160, true, 4)
+VITATTN_DKDV_INSTANTIATE(128, false, 4, 1)
+VITATTN_DKDV_INSTANTIATE(64, false, 4, 2)
+VITATTN_DKDV_INSTANTIATE(96, false, 4, 1)
+VITATTN_DKDV_INSTANTIATE(160, false, 4, 1)
+VITATTN_DKDV_INSTANTIATE(128, true, 4, 1)
+VITATTN_DKDV_INSTANTIATE(64, true, 4, 1)
+VITATTN_DKDV_INSTANTIATE(96, true, 4, 1)
+VITATTN_DKDV_INSTANTIATE(160, true, 4, 1)
 #undef VITATTN_DKDV_INSTANTIATE
 
 template <int D, int NW, int RING>

@@ -4,12 +4,14 @@ two workgroups over the two halves of the query tiles, which add dK and dV
 into zeroed rows, while whole key blocks form the same two partial sums
 (the first stored at the midpoint), so the bits do not depend on the
 split. The shapes below put whole and split key blocks in one
-launch on a 256-CU part with one dK/dV workgroup per CU (B*H*ceil(N/128)
-work items: 257 -> 256 whole + 1 split, 600 -> 512 + 88, 280 -> 256 + 24,
-260 -> 256 + 4 with 65 query tiles per half), including an odd tile count
-(the second half one tile longer) and a ragged last tile. Both backward
-modes, against the fp64 oracle; on any other device the same comparisons
-hold whatever the split."""
+launch on a 256-CU part with one dK/dV workgroup per CU (B*H*ceil(N/BK)
+work items, BK = 128 keys, or 256 at head dims up to 64 in the recompute
+mode: 257 -> 256 whole + 1 split, 600 -> 512 + 88, 280 -> 256 + 24, 260 ->
+256 + 4 with 130 query tiles per half, the last one ragged, and in the last
+work item a wave whose first 32-key block holds 24 keys and whose second
+lies past the end), including an odd tile count (the second half one tile
+longer). Both backward modes, against the fp64 oracle;
+on any other device the same comparisons hold whatever the split."""
 import numpy as np
 import pytest
 
@@ -19,7 +21,7 @@ from gpu_util import assert_close, run_hip, torch
 
 pytestmark = pytest.mark.gpu
 
-CASES = [(1, 257, 256, 64), (1, 300, 130, 128), (2, 70, 200, 160), (1, 4, 8320, 64), (1, 33, 1000, 96)]
+CASES = [(1, 257, 256, 64), (1, 300, 130, 128), (2, 70, 200, 160), (1, 4, 16600, 64), (1, 33, 1000, 96)]
 
 
 def np64(t):
@@ -52,9 +54,9 @@ def test_split_key_blocks_are_deterministic():
 
 @pytest.mark.parametrize("store_ds", [False, True], ids=["recompute", "stored-ds"])
 def test_head_alone_and_among_others(store_ds):
-    # N = 25,600 gives 200 key blocks per head: a head alone is 200 work items
-    # (no split on a 256-CU part), three heads are 600 (the last 88, all of
-    # head 2, split). Every key block sums its query tiles as the same two
+    # N = 25,600 at d = 64 gives 100 key blocks of 256 per head: a head alone
+    # is 100 work items (all split on a 256-CU part), three heads are 300
+    # (the last 44, all of head 2, split; head 2's first 56 whole). Every key block sums its query tiles as the same two
     # rounded partials whether it is split or whole, so all five outputs of
     # head 2 are bitwise equal (the check of Sec. VI-A that every process
     # computes the same matrices, here across call shapes).
@@ -69,7 +71,7 @@ def test_head_alone_and_among_others(store_ds):
         assert t.equal(full[name][:, 2:3], alone[name]), name
 
 
-@pytest.mark.parametrize("B,H,N,d", [(1, 300, 130, 128), (1, 4, 8320, 64), (1, 33, 1000, 96), (2, 70, 200, 160)])
+@pytest.mark.parametrize("B,H,N,d", [(1, 300, 130, 128), (1, 4, 16600, 64), (1, 33, 1000, 96), (2, 70, 200, 160)])
 def test_split_blocks_bitwise_equal_to_single_head_calls(B, H, N, d):
     # every head of a launch whose last round splits (see CASES) against the
     # same head in a call of its own, where the grid is far from a whole

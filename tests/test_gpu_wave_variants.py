@@ -1,10 +1,12 @@
 """At the narrowest tile (head dims up to 64) the forward and dQ kernels
-choose between 8- and 12-wave workgroups from the grid size, and the dK/dV
-kernel runs six 32-key blocks per workgroup. B=1, H=6, N=22,001 makes the
-six-head call take the 12-wave forward and dQ on a 256-CU part (two rounds
-of 384-query workgroups instead of three of 256) while each single-head call
-takes the 8-wave ones; every output must be bitwise equal between the two, and
-sampled query and key rows must match the fp64 oracle."""
+choose between 8- and 12-wave workgroups from the grid size, and each dK/dV
+wave holds two 32-key blocks (256 keys per workgroup). B=1, H=6, N=22,001
+makes the six-head call take the 12-wave forward and dQ on a 256-CU part
+(two rounds of 384-query workgroups instead of three of 256) while each
+single-head call takes the 8-wave ones, and splits 4 of its 516 dK/dV key
+blocks where a single-head call splits all 86; every output must be bitwise
+equal between the two, and sampled query and key rows must match the fp64
+oracle."""
 import numpy as np
 import pytest
 
