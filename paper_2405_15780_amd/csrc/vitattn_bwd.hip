@@ -101,9 +101,11 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 // slot index is then a compile-time constant (LDS addresses fold into
 // instruction immediates).
 //
-// Each wave's work per tile is one stream of 4*KPW*D/16 matrix-core ops whose
-// LDS operands are read two operands ahead, in four phases (query blocks 0,
-// 1; within a phase the KPW ops that share an operand are adjacent):
+// Each wave's work per tile is one stream of 2*KPW*(KS + D/16) matrix-core
+// ops whose LDS operands are read two operands ahead, in four phases (query
+// blocks 0, 1; within a phase the KPW ops that share an operand are
+// adjacent; the first products contract over the KS 16-column steps of d
+// that hold data, D/16 or 5 for d <= 80 in the 96-wide tile):
 //   1. first product of block 0 (S or dP)
 //   2. first product of block 1;  vector units: P or dS of block 0
 //   3. second product of block 0 (dV or dK);  vector units: block 1
@@ -121,7 +123,7 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 // own a key block and every query; the key blocks after them (at most half a
 // round of them) are split into two workgroups each, one per half of the
 // query tiles, which add their dK and dV into rows the launch zeroed first.
-template <int D, bool STORE_DS, int KBW, int KPW>
+template <int D, bool STORE_DS, int KBW, int KPW, int KS = D / 16>
 __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per_eu(KBW / 2, KBW / 2))) void attn_bwd_dkdv_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
@@ -129,8 +131,16 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
     const Map mv, const Map mg, const Map mdk, const Map mdv, int H, int dr, int Nq, int Nk, int n_ktiles,
     int n_whole, float c, float scale) {
   constexpr int KK = D / 16, NCB = D / 32;
-  constexpr int PH = KK;           // operands per phase (each feeding KPW ops)
-  constexpr int NA = 4 * PH;       // streamed operands per tile
+  static_assert(KS >= 1 && KS <= KK, "contraction steps within the tile");
+  // operands per phase (each feeding KPW ops): first products (S or dP)
+  // contract over d, second products (dV^T or dK^T) over 32 queries for each
+  // of the NCB 32-column blocks of d
+  constexpr int P1 = KS, P2 = KK;
+  constexpr int NA = 2 * P1 + 2 * P2;  // streamed operands per tile
+  constexpr int PMIN = P1 < P2 ? P1 : P2;
+  // phase of streamed operand a, and the first operand of phase ph
+  constexpr auto phase_of = [](int a) { return a < P1 ? 0 : a < 2 * P1 ? 1 : a < 2 * P1 + P2 ? 2 : 3; };
+  constexpr auto phase_start = [](int ph) { return ph < 2 ? ph * P1 : 2 * P1 + (ph - 2) * P2; };
   // query rows of vector work: row r rides on op slot r * PH / 16 of its phase
   constexpr int TILE_BYTES = kDkvBQ * D * 2;
   constexpr int RING = 3;
@@ -210,11 +220,11 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
   const Map& mh = role_p ? mk : mv;
   const int ldh = 2 * mh.ld;
   const rsrc_t rh = make_rsrc((role_p ? k : v) + mh.head(bh, H), (unsigned)(Nk * ldh));
-  bf16x8 hf[KPW][KK];
+  bf16x8 hf[KPW][KS];
 #pragma unroll
   for (int kp = 0; kp < KPW; ++kp)
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
+    for (int kk = 0; kk < KS; ++kk)
       hf[kp][kk] = as_bf16x8(buffer_load16(rh, chunk_offset(key0 + 32 * kp, 2 * kk + h, ldh, chr)));
 
   // Q and dO tiles. With STORE_DS only the four role-P waves fetch tiles, so
@@ -319,7 +329,7 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
 
     // streamed operand a (shared by the KPW ops of one phase slot)
     auto read_a = [&](int a) -> bf16x8 {
-      const int ph = a / PH, j = a % PH, qb = ph & 1;
+      const int ph = phase_of(a), j = a - phase_start(ph), qb = ph & 1;
       if (ph < 2) return lds_frag_row(RP ? qs : gs, qb * 32 * 2 * D + rf.at(j));
       return tf.load(RP ? gs : qs, qb * 32 + 16 * (j / NCB), j % NCB);
     };
@@ -336,13 +346,13 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
         }
       }
     };
-    auto valu = [&](int kp, int qb, int u) {
-      // rows u*16/PH .. (u+1)*16/PH - 1 (PH = 4 or 8: 16/PH rows per slot)
-      constexpr int RMAX = (16 + PH - 1) / PH;
+    auto valu = [&](int kp, int qb, int u, int ns) {
+      // slot u of ns: rows ceil(16 u / ns) .. ceil(16 (u + 1) / ns) - 1
+      constexpr int RMAX = (16 + PMIN - 1) / PMIN;
 #pragma unroll
       for (int rr = 0; rr < RMAX; ++rr) {
-        const int r = (u * 16 + PH - 1) / PH + rr;
-        if (r >= ((u + 1) * 16 + PH - 1) / PH) break;
+        const int r = (u * 16 + ns - 1) / ns + rr;
+        if (r >= ((u + 1) * 16 + ns - 1) / ns) break;
         const int sb = LEAN ? 0 : qb;
         const float sv = stat[sb][r >> 2][r & 3];
         float x;
@@ -375,16 +385,16 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
     static_for<0, NA * KPW>([&](auto IC) __attribute__((always_inline)) {
       constexpr int i = decltype(IC)::value;
       constexpr int a = i / KPW, kp = i % KPW;  // operand, key block
-      constexpr int ph = a / PH, j = a % PH, qb = ph & 1;
+      constexpr int ph = phase_of(a), j = a - phase_start(ph), qb = ph & 1;
       if constexpr (kp == 0 && a + AH < NA) aq[(a + AH) % (AH + 1)] = read_a(a + AH);
       if constexpr (ph < 2) {
         if constexpr (j == 0) m1[kp][qb] = zero16();
         m1[kp][qb] = mfma32(aq[a % (AH + 1)], hf[kp][j], m1[kp][qb]);
-        if constexpr (ph == 1) valu(kp, 0, j);
-        if constexpr (LEAN && i == 2 * PH * KPW - 1) read_side(1);
+        if constexpr (ph == 1) valu(kp, 0, j, P1);
+        if constexpr (LEAN && i == 2 * P1 * KPW - 1) read_side(1);
       } else {
         acc[kp][j % NCB] = mfma32(aq[a % (AH + 1)], ob[kp][qb][j / NCB], acc[kp][j % NCB]);
-        if constexpr (ph == 2) valu(kp, 1, j);
+        if constexpr (ph == 2) valu(kp, 1, j, P2);
       }
       sched_fence();
     });
@@ -587,8 +597,10 @@ __global__ __launch_bounds__(256) void zero_key_blocks_kernel(float* __restrict_
 // The tile loop is unrolled by the ring depth, so slots are compile-time
 // constants and LDS addresses fold into instruction immediates. Key rows
 // past the end arrive as zeros: their P is finite and they add
-// K_row^T dS = 0 to dQ, so no masking is needed.
-template <int D, int NW>
+// K_row^T dS = 0 to dQ, so no masking is needed. S and dP contract over the
+// KS 16-column steps of d that hold data (D/16, or 5 for d <= 80 in the
+// 96-wide tile).
+template <int D, int NW, int KS = D / 16>
 __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4))) void attn_bwd_dq_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lse2,
@@ -597,7 +609,8 @@ __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu
   constexpr int BM = 32 * NW;
   constexpr int BN = 32;
   constexpr int KK = D / 16, NCB = D / 32;
-  constexpr int NS = 2 * KK;       // S and dP ops per tile
+  static_assert(KS >= 1 && KS <= KK, "contraction steps within the tile");
+  constexpr int NS = 2 * KS;       // S and dP ops per tile
   constexpr int NQ = KK;           // dQ ops per tile (2 contraction steps x NCB)
   constexpr int TILE_BYTES = BN * D * 2;
   constexpr int RING = 6;
@@ -635,9 +648,9 @@ __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu
   const rsrc_t rv = make_rsrc(v + mv.head(bh, H), (unsigned)(Nk * ldv));
 
   const int qrow = qt * BM + wave * 32 + (lane & 31);
-  bf16x8 qf[KK], gf[KK];
+  bf16x8 qf[KS], gf[KS];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
+  for (int kk = 0; kk < KS; ++kk) {
     qf[kk] = as_bf16x8(buffer_load16(rq, chunk_offset(qrow, 2 * kk + h, ldq, chr)));
     gf[kk] = as_bf16x8(buffer_load16(rg, chunk_offset(qrow, 2 * kk + h, ldg, chr)));
   }
@@ -671,9 +684,9 @@ __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu
   f32x16 sa[2], sb[2];  // [S^T, dP^T] of the current and the next tile
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
-    if (i % KK == 0) sa[i / KK] = zero16();
-    sa[i / KK] = mfma32(lds_frag_row(i < KK ? kbuf[0] : vbuf[0], rf.at(i % KK)), i < KK ? qf[i] : gf[i - KK],
-                        sa[i / KK]);
+    if (i % KS == 0) sa[i / KS] = zero16();
+    sa[i / KS] = mfma32(lds_frag_row(i < KS ? kbuf[0] : vbuf[0], rf.at(i % KS)), i < KS ? qf[i] : gf[i - KS],
+                        sa[i / KS]);
   }
 
   // Stage j with SL = j % RING known at compile time: P, dS of tile j (from
@@ -706,8 +719,8 @@ __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu
       constexpr int W = NS + NCB - 1;
       static_assert(7 * W / 16 <= NS - 2 && 15 * W / 16 <= NS + NCB - 2, "dS ready before its dQ op");
       auto load_op = [&](int i) -> bf16x8 {
-        if (i < KK) return lds_frag_row(kbuf[NX], rf.at(i));
-        if (i < NS) return lds_frag_row(vbuf[NX], rf.at(i - KK));
+        if (i < KS) return lds_frag_row(kbuf[NX], rf.at(i));
+        if (i < NS) return lds_frag_row(vbuf[NX], rf.at(i - KS));
         const int t = i - NS;
         return tf.load(ks, 16 * (t / NCB), t % NCB);
       };
@@ -718,11 +731,11 @@ __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu
         constexpr int i = decltype(IC)::value;
         if constexpr (i + 1 < NOPS) aq[(i + 1) & 1] = load_op(i + 1);
         if constexpr (i < NS) {
-          if constexpr (i % KK == 0) nxt[i / KK] = zero16();
-          if constexpr (i < KK)
+          if constexpr (i % KS == 0) nxt[i / KS] = zero16();
+          if constexpr (i < KS)
             nxt[0] = mfma32(aq[i & 1], qf[i], nxt[0]);
           else
-            nxt[1] = mfma32(aq[i & 1], gf[i - KK], nxt[1]);
+            nxt[1] = mfma32(aq[i & 1], gf[i - KS], nxt[1]);
         } else {
           constexpr int t = i - NS;
           dqacc[t % NCB] = mfma32(aq[i & 1], dsb[t / NCB], dqacc[t % NCB]);
@@ -991,7 +1004,7 @@ static hipError_t rowdot_l(const BwdArgs& a) {
 
 // Workgroups of the dK/dV kernel resident on the current device at once
 // (0 if the runtime cannot say), looked up once per device.
-template <int D, bool STORE_DS, int KBW, int KPW>
+template <int D, bool STORE_DS, int KBW, int KPW, int KS>
 static int dkdv_resident_workgroups() {
   static std::atomic<int> known[64];  // per device ordinal; 0 = not looked up, -1 = unknown
   int dev = 0;
@@ -1000,7 +1013,7 @@ static int dkdv_resident_workgroups() {
   if (n == 0) {
     int per_cu = 0, cus = 0;
     n = -1;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dkdv_kernel<D, STORE_DS, KBW, KPW>,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dkdv_kernel<D, STORE_DS, KBW, KPW, KS>,
                                                      128 * KBW, 0) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && per_cu * cus > 0)
       n = per_cu * cus;
@@ -1009,14 +1022,14 @@ static int dkdv_resident_workgroups() {
   return n > 0 ? n : 0;
 }
 
-template <int D, bool STORE_DS, int KBW, int KPW>
+template <int D, bool STORE_DS, int KBW, int KPW, int KS = D / 16>
 static hipError_t dkdv_s(const BwdArgs& a) {
   constexpr int BK = 32 * KBW * KPW;
   const int n_kt = (a.Nk + BK - 1) / BK;
   const int total = a.BH * n_kt;
   // A last round at most half full is split in two halves of the query range
   // (when there are two query tiles to split), so that it takes half as long.
-  const int slots = dkdv_resident_workgroups<D, STORE_DS, KBW, KPW>();
+  const int slots = dkdv_resident_workgroups<D, STORE_DS, KBW, KPW, KS>();
   const int tail = slots > 0 ? total % slots : 0;
   int n_whole = total;
   if (tail > 0 && 2 * tail <= slots && (a.Nq + kDkvBQ - 1) / kDkvBQ >= 2) {
@@ -1025,7 +1038,7 @@ static hipError_t dkdv_s(const BwdArgs& a) {
                        a.d, a.Nk, n_kt, n_whole, BK);
   }
   const int grid = n_whole + 2 * (total - n_whole);
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS, KBW, KPW>), dim3(grid), dim3(64 * 2 * KBW), 0, a.stream, a.q,
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, STORE_DS, KBW, KPW, KS>), dim3(grid), dim3(64 * 2 * KBW), 0, a.stream, a.q,
                      a.k, a.v, a.dout, a.drow, a.lse2, a.dk, a.dv, a.ds, a.mq, a.mk, a.mv, a.mg, a.mdk, a.mdv, a.H,
                      a.d, a.Nq, a.Nk, n_kt, n_whole, a.scale * kLog2e, a.scale);
   return hipGetLastError();
@@ -1038,27 +1051,33 @@ static hipError_t dkdv_s(const BwdArgs& a) {
 // N=188,416, d=64), with the same bits. At the wider tiles two blocks per
 // wave leave room for one wave per SIMD only, which measured 5 % slower at
 // d=128 and no faster at d=96. The dS mode keeps one block per wave (its
-// stored dS blocks are laid out per 128 keys).
+// stored dS blocks are laid out per 128 keys). In the 96-wide tile a head
+// dim up to 80 contracts S and dP over five 16-column steps instead of six.
 template <int D>
 static hipError_t dkdv_d(const BwdArgs& a) {
+  if constexpr (D == 96) {
+    if (a.d <= 80) return a.ds != nullptr ? dkdv_s<96, true, 4, 1, 5>(a) : dkdv_s<96, false, 4, 1, 5>(a);
+  }
   if (a.ds != nullptr) return dkdv_s<D, true, 4, 1>(a);
   return dkdv_s<D, false, 4, D == 64 ? 2 : 1>(a);
 }
 
-#define VITATTN_DKDV_INSTANTIATE(D, S, KBW, KPW)                                                               \
-  template __global__ void attn_bwd_dkdv_kernel<D, S, KBW, KPW>(                                              \
+#define VITATTN_DKDV_INSTANTIATE(D, S, KBW, KPW, KS)                                                           \
+  template __global__ void attn_bwd_dkdv_kernel<D, S, KBW, KPW, KS>(                                          \
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
       float* __restrict__, uint16_t* __restrict__, const Map, const Map, const Map, const Map, const Map,      \
       const Map, int, int, int, int, int, int, float, float);
-VITATTN_DKDV_INSTANTIATE(128, false, 4, 1)
-VITATTN_DKDV_INSTANTIATE(64, false, 4, 2)
-VITATTN_DKDV_INSTANTIATE(96, false, 4, 1)
-VITATTN_DKDV_INSTANTIATE(160, false, 4, 1)
-VITATTN_DKDV_INSTANTIATE(128, true, 4, 1)
-VITATTN_DKDV_INSTANTIATE(64, true, 4, 1)
-VITATTN_DKDV_INSTANTIATE(96, true, 4, 1)
-VITATTN_DKDV_INSTANTIATE(160, true, 4, 1)
+VITATTN_DKDV_INSTANTIATE(128, false, 4, 1, 8)
+VITATTN_DKDV_INSTANTIATE(64, false, 4, 2, 4)
+VITATTN_DKDV_INSTANTIATE(96, false, 4, 1, 6)
+VITATTN_DKDV_INSTANTIATE(96, false, 4, 1, 5)
+VITATTN_DKDV_INSTANTIATE(160, false, 4, 1, 10)
+VITATTN_DKDV_INSTANTIATE(128, true, 4, 1, 8)
+VITATTN_DKDV_INSTANTIATE(64, true, 4, 1, 4)
+VITATTN_DKDV_INSTANTIATE(96, true, 4, 1, 6)
+VITATTN_DKDV_INSTANTIATE(96, true, 4, 1, 5)
+VITATTN_DKDV_INSTANTIATE(160, true, 4, 1, 10)
 #undef VITATTN_DKDV_INSTANTIATE
 
 template <int D, int NW, int RING>
@@ -1087,26 +1106,27 @@ VITATTN_DQDS_INSTANTIATE(128, 8, 6)
 VITATTN_DQDS_INSTANTIATE(160, 8, 6)
 #undef VITATTN_DQDS_INSTANTIATE
 
-template <int D, int NW>
+template <int D, int NW, int KS = D / 16>
 static hipError_t dq_v(const BwdArgs& a) {
   const int n_qt = (a.Nq + 32 * NW - 1) / (32 * NW);
   const int total = a.BH * n_qt;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v, a.dout,
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, NW, KS>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v, a.dout,
                      a.drow, a.lse2, a.dq, a.mq, a.mk, a.mv, a.mg, a.mdq, a.H, a.d, a.Nq, a.Nk, n_qt, total,
                      a.scale * kLog2e, a.scale, a.accumulate_dq ? 1 : 0);
   return hipGetLastError();
 }
 
-#define VITATTN_DQ_INSTANTIATE(D, NW)                                                                          \
-  template __global__ void attn_bwd_dq_kernel<D, NW>(                                                         \
+#define VITATTN_DQ_INSTANTIATE(D, NW, KS)                                                                      \
+  template __global__ void attn_bwd_dq_kernel<D, NW, KS>(                                                     \
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
       const uint16_t* __restrict__, const float* __restrict__, const float* __restrict__, float* __restrict__, \
       const Map, const Map, const Map, const Map, const Map, int, int, int, int, int, int, float, float, int);
-VITATTN_DQ_INSTANTIATE(128, 8)
-VITATTN_DQ_INSTANTIATE(64, 8)
-VITATTN_DQ_INSTANTIATE(64, 12)
-VITATTN_DQ_INSTANTIATE(96, 8)
-VITATTN_DQ_INSTANTIATE(160, 8)
+VITATTN_DQ_INSTANTIATE(128, 8, 8)
+VITATTN_DQ_INSTANTIATE(64, 8, 4)
+VITATTN_DQ_INSTANTIATE(64, 12, 4)
+VITATTN_DQ_INSTANTIATE(96, 8, 6)
+VITATTN_DQ_INSTANTIATE(96, 8, 5)
+VITATTN_DQ_INSTANTIATE(160, 8, 10)
 #undef VITATTN_DQ_INSTANTIATE
 
 hipError_t launch_bwd_rowdot(const BwdArgs& a) {
@@ -1167,7 +1187,7 @@ hipError_t launch_bwd_dq(const BwdArgs& a) {
   if (a.ds != nullptr) return launch_bwd_dq_ds(a);
   switch (tile_width(a.d)) {
     case 64: return dq_64(a);
-    case 96: return dq_v<96, 8>(a);
+    case 96: return a.d <= 80 ? dq_v<96, 8, 5>(a) : dq_v<96, 8>(a);  // d <= 80: five contraction steps
     case 128: return dq_v<128, 8>(a);
     default: return dq_v<160, 8>(a);
   }

@@ -15,7 +15,9 @@
 // Operands may have any batch / head / row strides (rows 16-byte aligned): the
 // kernel only forms addresses from them. The tile width D is 64, 96, 128 or
 // 160; for a head dim d below D the columns past d are loaded as zeros (they
-// add nothing to the scores) and never stored.
+// add nothing to the scores) and never stored. The scores contract over the
+// KS 16-column steps of d that hold data (D/16, or 5 for d <= 80 in the
+// 96-wide tile): the steps past them would add exact zeros.
 //
 // Software pipeline across tiles: the scores of tile j+1 are computed on the
 // matrix cores while the vector units turn tile j's scores into
@@ -66,7 +68,7 @@ constexpr int exp_window(int NS, int CPB, int KB, int NOPS) {
   return w;
 }
 
-template <int D, int KB, int NW, int MINW>
+template <int D, int KB, int NW, int MINW, int KS = D / 16>
 __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t* __restrict__ q,
                                                                  const uint16_t* __restrict__ k,
                                                                  const uint16_t* __restrict__ v,
@@ -77,7 +79,8 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   constexpr int BM = 32 * NW;  // query rows per workgroup
   constexpr int BN = 32 * KB;  // keys per tile
   constexpr int TILE_BYTES = BN * D * 2;
-  constexpr int KK = D / 16;           // contraction steps of one 32-key score block
+  constexpr int KK = KS;               // contraction steps of one 32-key score block
+  static_assert(KS >= 1 && KS <= D / 16, "contraction steps within the tile");
   constexpr int NS = KB * KK;          // score ops per tile
   constexpr int NV = 2 * KB * D / 32;  // PV ops per tile
   // One variable per ring slot: the compiler then knows that reading one
@@ -316,13 +319,13 @@ __global__ __launch_bounds__(64 * NW, MINW) void attn_fwd_kernel(const uint16_t*
   }
 }
 
-template <int D, int KB, int NW, int MINW>
+template <int D, int KB, int NW, int MINW, int KS = D / 16>
 static hipError_t launch_fwd_v(const FwdArgs& a) {
   constexpr int BM = 32 * NW;
   const int n_qtiles = (a.Nq + BM - 1) / BM;
   const int total = a.BH * n_qtiles;
   const float c = a.scale * kLog2e;
-  hipLaunchKernelGGL((attn_fwd_kernel<D, KB, NW, MINW>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v,
+  hipLaunchKernelGGL((attn_fwd_kernel<D, KB, NW, MINW, KS>), dim3(total), dim3(64 * NW), 0, a.stream, a.q, a.k, a.v,
                      a.o, a.lse, a.mq, a.mk, a.mv, a.mo, a.H, a.d, a.Nq, a.Nk, n_qtiles, total, c);
   return hipGetLastError();
 }
@@ -330,9 +333,10 @@ static hipError_t launch_fwd_v(const FwdArgs& a) {
 // Every tile variant is instantiated explicitly: hipcc otherwise omits the
 // host-side launch stub of some instantiations reached only through this
 // dispatch, and the library then fails to load.
-#define VITATTN_FWD_VARIANTS(X) X(128, 2, 8, 2) X(64, 2, 8, 2) X(64, 2, 12, 3) X(96, 2, 8, 2) X(160, 1, 8, 2)
-#define VITATTN_FWD_INSTANTIATE(D, KB, NW, MINW)                                                               \
-  template __global__ void attn_fwd_kernel<D, KB, NW, MINW>(                                                  \
+#define VITATTN_FWD_VARIANTS(X) \
+  X(128, 2, 8, 2, 8) X(64, 2, 8, 2, 4) X(64, 2, 12, 3, 4) X(96, 2, 8, 2, 6) X(96, 2, 8, 2, 5) X(160, 1, 8, 2, 10)
+#define VITATTN_FWD_INSTANTIATE(D, KB, NW, MINW, KS)                                                           \
+  template __global__ void attn_fwd_kernel<D, KB, NW, MINW, KS>(                                              \
       const uint16_t* __restrict__, const uint16_t* __restrict__, const uint16_t* __restrict__,               \
       float* __restrict__, float* __restrict__, const Map, const Map, const Map, const Map, int, int, int, int, \
       int, int, float);
@@ -377,11 +381,13 @@ static hipError_t launch_fwd_64(const FwdArgs& a) {
 // Tile shape per width (key blocks per tile, waves per workgroup, waves per
 // SIMD): two 32-key blocks per tile and 8 waves x 32 queries, except at
 // D = 160, where one key block per tile keeps the registers within budget,
-// and at D = 64, where 12 waves are chosen when the grid allows (above).
+// and at D = 64, where 12 waves are chosen when the grid allows (above). In
+// the 96-wide tile a head dim up to 80 (ViT-10B's 72) contracts the scores
+// over five 16-column steps instead of six.
 hipError_t launch_fwd(const FwdArgs& a) {
   switch (tile_width(a.d)) {
     case 64: return launch_fwd_64(a);
-    case 96: return launch_fwd_v<96, 2, 8, 2>(a);
+    case 96: return a.d <= 80 ? launch_fwd_v<96, 2, 8, 2, 5>(a) : launch_fwd_v<96, 2, 8, 2>(a);
     case 128: return launch_fwd_v<128, 2, 8, 2>(a);
     default: return launch_fwd_v<160, 1, 8, 2>(a);
   }
