@@ -83,17 +83,43 @@ KERNEL_FILES = {
 }
 
 
-def kernel_sources_digest(row="attention"):
-    """Hash of the HIP sources that define one kernel family (plus the shared
-    headers), to tell whether stored counter readings still describe the
-    kernels being timed."""
+def strip_comments(src):
+    """C++ source without its comments and blank lines (string and character
+    literals kept as they are), so that editing a comment leaves the digest
+    below unchanged."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return "\n".join(line.rstrip() for line in "".join(out).splitlines() if line.strip())
+
+
+def kernel_sources_digest(row="attention", csrc=None):
+    """Hash of the code (comments stripped) of the HIP sources that define one
+    kernel family, plus the shared headers, to tell whether stored counter
+    readings still describe the kernels being timed."""
     import hashlib
 
-    csrc = os.path.join(ROOT, "paper_2405_15780_amd", "csrc")
+    csrc = csrc or os.path.join(ROOT, "paper_2405_15780_amd", "csrc")
     h = hashlib.sha256()
     for name in sorted(KERNEL_FILES[row] + ("vitattn_common.h", "vitattn_launch.h")):
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
+        with open(os.path.join(csrc, name), encoding="utf-8") as f:
+            h.update(name.encode() + b"\0" + strip_comments(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -141,7 +141,6 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
   // phase of streamed operand a, and the first operand of phase ph
   constexpr auto phase_of = [](int a) { return a < P1 ? 0 : a < 2 * P1 ? 1 : a < 2 * P1 + P2 ? 2 : 3; };
   constexpr auto phase_start = [](int ph) { return ph < 2 ? ph * P1 : 2 * P1 + (ph - 2) * P2; };
-  // query rows of vector work: row r rides on op slot r * PH / 16 of its phase
   constexpr int TILE_BYTES = kDkvBQ * D * 2;
   constexpr int RING = 3;
   constexpr int NWAVES = 2 * KBW;

@@ -72,3 +72,25 @@ def test_clock_summary_ignores_idle_samples():
     s.samples = [(253.0, 157.0), (1300.0, 1900.0), (1320.0, 2000.0)]
     got = s.summary()
     assert got["samples"] == 2 and got["sclk_mhz_min"] == 1900.0 and got["power_w_median"] == 1310.0
+
+
+def test_source_digest_ignores_comments_but_not_code(tmp_path):
+    # stored counter readings stay valid across comment edits and are
+    # invalidated by any change to the code they were taken on
+    import shutil
+
+    sys.path.insert(0, ROOT)
+    import bench
+
+    src = os.path.join(ROOT, "paper_2405_15780_amd", "csrc")
+    for name in os.listdir(src):
+        shutil.copy(os.path.join(src, name), tmp_path / name)
+    base = bench.kernel_sources_digest("attention", str(tmp_path))
+    assert base == bench.kernel_sources_digest("attention")
+    path = tmp_path / "vitattn_bwd.hip"
+    code = path.read_text()
+    path.write_text("// a new comment line\n" + code.replace("\n}", "  /* inline */\n}", 1) + "\n\n// trailing\n")
+    assert bench.kernel_sources_digest("attention", str(tmp_path)) == base
+    path.write_text(code.replace("constexpr int RING = 3;", "constexpr int RING = 4;", 1))
+    assert bench.kernel_sources_digest("attention", str(tmp_path)) != base
+    assert bench.strip_comments('a = "//x"; // c\nb = 1; /* d */ c\n\n') == 'a = "//x";\nb = 1;   c'
