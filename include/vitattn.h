@@ -115,7 +115,8 @@ int vitattn_bwd(const void* q, const void* k, const void* v, const float* o, con
  * The three stages of vitattn_bwd, callable one by one (same arguments,
  * layouts and validation as vitattn_bwd; used to time each kernel). They
  * must run in this order on one stream, all with the same workspace:
- *   vitattn_bwd_rowdot: workspace <- D_i = sum_c dout_ic o_ic and LSE_i*log2(e);
+ *   vitattn_bwd_rowdot: workspace <- -D_i = -sum_c dout_ic o_ic (stored negated)
+ *                       and LSE_i*log2(e);
  *   vitattn_bwd_dkdv  : dk, dv from q, k, v, dout, lse and D in the workspace;
  *   vitattn_bwd_dq    : dq from q, k, v, dout, lse and D in the workspace.
  * Each stage validates its own arguments like vitattn_bwd does.

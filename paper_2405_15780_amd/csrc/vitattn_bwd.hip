@@ -31,9 +31,10 @@ namespace vitattn {
 
 // ------------------------------------------------------------------ preprocess
 
-// Writes the two per-row statistics the backward kernels stream: D_i =
-// sum_c dO_ic O_ic and LSE_i * log2(e) (the logsumexp in the base-2 units of
-// the kernels' exp2). Each lives in its own region of the workspace. LPR
+// Writes the two per-row statistics the backward kernels stream: -D_i =
+// -sum_c dO_ic O_ic (negated, so that the dK/dV kernel can start its dP
+// accumulator at it) and LSE_i * log2(e) (the logsumexp in the base-2 units
+// of the kernels' exp2). Each lives in its own region of the workspace. LPR
 // lanes per row take 8 columns each (lanes past the head dim add nothing).
 template <int LPR>
 __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __restrict__ dout,
@@ -58,7 +59,7 @@ __global__ __launch_bounds__(256) void attn_bwd_rowdot_kernel(const uint16_t* __
 #pragma unroll
   for (int m = LPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
   if (row < rows && part == 0) {
-    drow[row] = acc;
+    drow[row] = -acc;
     lse2[row] = lse[row] * kLog2e;
   }
 }
@@ -310,7 +311,11 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
   // reads has to wait for that DMA. The widest tile, and waves with more than
   // one key block, have no registers to spare for both blocks: there block
   // 1's are read into block 0's registers once block 0's vector work is done
-  // (end of phase 2).
+  // (end of phase 2). Role dS starts each dP accumulator at the block's -D
+  // (its 16 statistics per lane sit in the accumulator's row order), so dP -
+  // D leaves the matrix cores; it then needs block 1's statistics from the
+  // start and reads only block 1's P late. The widest tile keeps the
+  // subtraction on the vector units.
   auto run_tile = [&](auto role_tag, auto slot_tag, int tile, auto&& prefetch) {
     constexpr bool RP = decltype(role_tag)::value;
     constexpr int SL = decltype(slot_tag)::value;
@@ -322,8 +327,11 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
     f32x16 m1[KPW][2];     // S (P) or dP (dS), per key block and query block
     bf16x8 ob[KPW][2][2];  // bf16 operands of P or dS [key block][query block][contraction step]
     constexpr bool LEAN = D == 160 || KPW > 1;
-    constexpr int NSB = LEAN ? 1 : 2;  // query blocks whose side data is held at once
-    float4 stat[NSB][4];   // LSE2 (role P) or D (role dS) of the block's rows
+    constexpr bool DINIT = !RP && D != 160;      // dP accumulators start at -D
+    constexpr bool LEAN_STAT = LEAN && !DINIT;   // statistics of one query block at a time
+    constexpr int NSB = LEAN ? 1 : 2;  // query blocks whose P (role dS) is held at once
+    constexpr int NST = LEAN_STAT ? 1 : 2;  // ... whose statistics are held at once
+    float4 stat[NST][4];   // LSE2 (role P) or -D (role dS) of the block's rows
     uint4 pin4[KPW][NSB][2];  // role dS: the partner's P, as bf16 pairs
 
     // streamed operand a (shared by the KPW ops of one phase slot)
@@ -332,11 +340,27 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
       if (ph < 2) return lds_frag_row(RP ? qs : gs, qb * 32 * 2 * D + rf.at(j));
       return tf.load(RP ? gs : qs, qb * 32 + 16 * (j / NCB), j % NCB);
     };
-    auto read_side = [&](int qb) {
-      const int sb = LEAN ? 0 : qb;
+    auto read_stat = [&](int qb) {
 #pragma unroll
       for (int g = 0; g < 4; ++g)
-        stat[sb][g] = *reinterpret_cast<const float4*>(st + (RP ? kDkvBQ : 0) + qb * 32 + 8 * g + 4 * h);
+        stat[LEAN_STAT ? 0 : qb][g] = *reinterpret_cast<const float4*>(st + (RP ? kDkvBQ : 0) + qb * 32 + 8 * g + 4 * h);
+    };
+    // the 16 statistics of query block qb in accumulator order (row 8g + 4h + e
+    // in element 4g + e)
+    auto stat_acc = [&](int qb) {
+      f32x16 v;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 t = stat[LEAN_STAT ? 0 : qb][g];
+        v[4 * g] = t.x;
+        v[4 * g + 1] = t.y;
+        v[4 * g + 2] = t.z;
+        v[4 * g + 3] = t.w;
+      }
+      return v;
+    };
+    auto read_p = [&](int qb) {
+      const int sb = LEAN ? 0 : qb;
       if constexpr (!RP) {
 #pragma unroll
         for (int kp = 0; kp < KPW; ++kp) {
@@ -353,14 +377,17 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
         const int r = (u * 16 + ns - 1) / ns + rr;
         if (r >= ((u + 1) * 16 + ns - 1) / ns) break;
         const int sb = LEAN ? 0 : qb;
-        const float sv = stat[sb][r >> 2][r & 3];
+        const float sv = stat[LEAN_STAT ? 0 : qb][r >> 2][r & 3];
         float x;
         if constexpr (RP) {
           x = __builtin_amdgcn_exp2f(__builtin_fmaf(m1[kp][qb][r], c, -sv));
         } else {
           const unsigned w = pin4[kp][sb][r >> 3][(r & 7) >> 1];
           const float p = __uint_as_float((r & 1) ? (w & 0xffff0000u) : (w << 16));
-          x = p * (m1[kp][qb][r] - sv);
+          if constexpr (DINIT)
+            x = p * m1[kp][qb][r];  // dP - D from the matrix cores
+          else
+            x = p * (m1[kp][qb][r] + sv);
         }
         pin(x);
         m1[kp][qb][r] = x;
@@ -369,8 +396,10 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
     };
 
     if constexpr (!RP) flush_ds();  // the previous tile's dS, before this tile's DMA requests
-    read_side(0);
-    if constexpr (!LEAN) read_side(1);
+    read_stat(0);
+    read_p(0);
+    if constexpr (!LEAN_STAT) read_stat(1);
+    if constexpr (!LEAN) read_p(1);
     constexpr int AH = kDkvAhead;  // operand reads run AH operands ahead of their matrix-core ops
     bf16x8 aq[AH + 1];
 #pragma unroll
@@ -387,10 +416,19 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
       constexpr int ph = phase_of(a), j = a - phase_start(ph), qb = ph & 1;
       if constexpr (kp == 0 && a + AH < NA) aq[(a + AH) % (AH + 1)] = read_a(a + AH);
       if constexpr (ph < 2) {
-        if constexpr (j == 0) m1[kp][qb] = zero16();
-        m1[kp][qb] = mfma32(aq[a % (AH + 1)], hf[kp][j], m1[kp][qb]);
+        if constexpr (j == 0) {
+          if constexpr (DINIT)
+            m1[kp][qb] = mfma32(aq[a % (AH + 1)], hf[kp][j], stat_acc(qb));
+          else
+            m1[kp][qb] = mfma32(aq[a % (AH + 1)], hf[kp][j], zero16());
+        } else {
+          m1[kp][qb] = mfma32(aq[a % (AH + 1)], hf[kp][j], m1[kp][qb]);
+        }
         if constexpr (ph == 1) valu(kp, 0, j, P1);
-        if constexpr (LEAN && i == 2 * P1 * KPW - 1) read_side(1);
+        if constexpr (LEAN && i == 2 * P1 * KPW - 1) {
+          if constexpr (LEAN_STAT) read_stat(1);
+          read_p(1);
+        }
       } else {
         acc[kp][j % NCB] = mfma32(aq[a % (AH + 1)], ob[kp][qb][j / NCB], acc[kp][j % NCB]);
         if constexpr (ph == 2) valu(kp, 1, j, P2);
@@ -657,7 +695,7 @@ __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu
   const rsrc_t rd = make_rsrc(drow + (size_t)bh * Nq, (unsigned)Nq * 4);
   // (the b32 buffer load returns the raw bits)
   const float l2 = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, qrow * 4, 0, 0));
-  const float dval = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, qrow * 4, 0, 0));
+  const float dval = -__builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, qrow * 4, 0, 0));  // stored -D
 
   TileDma<D, BN, NW> dma, dmv;  // K and V tiles
   dma.init(wave, lane, ldk, chr);
