@@ -1080,20 +1080,23 @@ static hipError_t dkdv_s(const BwdArgs& a) {
                      a.d, a.Nq, a.Nk, n_kt, n_whole, a.scale * kLog2e, a.scale);
   return hipGetLastError();
 }
-// Four pairs of waves per workgroup. At the narrowest tile in the recompute
-// mode each wave holds two 32-key blocks (234 VGPRs, two waves per SIMD, 256
-// keys per workgroup), so every operand it reads from LDS feeds two
-// matrix-core ops and every Q / dO tile it streams serves twice the keys:
-// 8 % faster than six one-block pairs at three waves per SIMD (B=4, H=1,
-// N=188,416, d=64), with the same bits. At the wider tiles two blocks per
-// wave leave room for one wave per SIMD only, which measured 5 % slower at
-// d=128 and no faster at d=96. The dS mode keeps one block per wave (its
-// stored dS blocks are laid out per 128 keys). In the 96-wide tile a head
-// dim up to 80 contracts S and dP over five 16-column steps instead of six.
+// Four pairs of waves per workgroup, except where noted. At the narrowest
+// tile in the recompute mode each wave holds two 32-key blocks (222 VGPRs,
+// two waves per SIMD, 256 keys per workgroup), so every operand it reads
+// from LDS feeds two matrix-core ops and every Q / dO tile it streams serves
+// twice the keys: 8 % faster than six one-block pairs at three waves per
+// SIMD (B=4, H=1, N=188,416, d=64), with the same bits. At the wider tiles
+// two blocks per wave leave room for one wave per SIMD only, which measured
+// 5 % slower at d=128 and no faster at d=96. In the 96-wide tile a head dim
+// up to 80 contracts S and dP over five 16-column steps instead of six, and
+// the recompute mode then fits three waves per SIMD (168 VGPRs, two values
+// spilled outside the tile loop): six pairs, 192 keys per workgroup, 4-5 %
+// faster at d=72 on large grids, with the same bits. The dS mode keeps four
+// pairs of one-block waves (its stored dS blocks are laid out per 128 keys).
 template <int D>
 static hipError_t dkdv_d(const BwdArgs& a) {
   if constexpr (D == 96) {
-    if (a.d <= 80) return a.ds != nullptr ? dkdv_s<96, true, 4, 1, 5>(a) : dkdv_s<96, false, 4, 1, 5>(a);
+    if (a.d <= 80) return a.ds != nullptr ? dkdv_s<96, true, 4, 1, 5>(a) : dkdv_s<96, false, 6, 1, 5>(a);
   }
   if (a.ds != nullptr) return dkdv_s<D, true, 4, 1>(a);
   return dkdv_s<D, false, 4, D == 64 ? 2 : 1>(a);
@@ -1108,7 +1111,7 @@ static hipError_t dkdv_d(const BwdArgs& a) {
 VITATTN_DKDV_INSTANTIATE(128, false, 4, 1, 8)
 VITATTN_DKDV_INSTANTIATE(64, false, 4, 2, 4)
 VITATTN_DKDV_INSTANTIATE(96, false, 4, 1, 6)
-VITATTN_DKDV_INSTANTIATE(96, false, 4, 1, 5)
+VITATTN_DKDV_INSTANTIATE(96, false, 6, 1, 5)
 VITATTN_DKDV_INSTANTIATE(160, false, 4, 1, 10)
 VITATTN_DKDV_INSTANTIATE(128, true, 4, 1, 8)
 VITATTN_DKDV_INSTANTIATE(64, true, 4, 1, 4)
@@ -1163,6 +1166,7 @@ VITATTN_DQ_INSTANTIATE(64, 8, 4)
 VITATTN_DQ_INSTANTIATE(64, 12, 4)
 VITATTN_DQ_INSTANTIATE(96, 8, 6)
 VITATTN_DQ_INSTANTIATE(96, 8, 5)
+VITATTN_DQ_INSTANTIATE(96, 12, 5)
 VITATTN_DQ_INSTANTIATE(160, 8, 10)
 #undef VITATTN_DQ_INSTANTIATE
 
@@ -1188,7 +1192,7 @@ hipError_t launch_bwd_dq_ds(const BwdArgs& a) {
 }
 // Workgroups of a dQ kernel variant resident on the current device at once
 // (0 if the runtime cannot say), looked up once per device.
-template <int D, int NW>
+template <int D, int NW, int KS>
 static int dq_resident_workgroups() {
   static std::atomic<int> known[64];
   int dev = 0;
@@ -1197,7 +1201,7 @@ static int dq_resident_workgroups() {
   if (n == 0) {
     int per_cu = 0, cus = 0;
     n = -1;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dq_kernel<D, NW>, 64 * NW, 0) == hipSuccess &&
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bwd_dq_kernel<D, NW, KS>, 64 * NW, 0) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && per_cu * cus > 0)
       n = per_cu * cus;
     known[dev].store(n, std::memory_order_relaxed);
@@ -1205,26 +1209,29 @@ static int dq_resident_workgroups() {
   return n > 0 ? n : 0;
 }
 
-// At the narrowest tile the dQ kernel's 168 VGPRs fit three waves per SIMD:
-// 12 waves (384 queries) per workgroup share each K / V tile, ~6 % faster per
-// query than 8 waves (measured at B=4, H=1, N=188,416), but in coarser work
-// items. The variant with the shorter estimated time (whole rounds of
-// resident workgroups x queries per workgroup / that rate) is launched; both
-// compute every dQ row with the same operations in the same order, so the
-// choice changes no bit.
-static hipError_t dq_64(const BwdArgs& a) {
-  const int s8 = dq_resident_workgroups<64, 8>(), s12 = dq_resident_workgroups<64, 12>();
-  if (s8 <= 0 || s12 <= 0) return dq_v<64, 8>(a);
+// At the narrowest tile (168 VGPRs) and at D = 96 with five contraction
+// steps (168, one 16-byte operand spilled and reloaded three times per six
+// tiles) the dQ kernel fits three waves per SIMD: 12 waves (384 queries) per workgroup share each K /
+// V tile, faster per query than 8 waves (~6 % at D = 64, B=4, H=1, N=188,416;
+// ~4.5 % at d = 72, B=1, H=2-3, N=50,001-188,416), but in coarser work items.
+// The variant with the shorter estimated time (whole rounds of resident
+// workgroups x queries per workgroup / that rate) is launched; both compute
+// every dQ row with the same operations in the same order, so the choice
+// changes no bit.
+template <int D, int KS>
+static hipError_t dq_8_or_12(const BwdArgs& a, double rate12) {
+  const int s8 = dq_resident_workgroups<D, 8, KS>(), s12 = dq_resident_workgroups<D, 12, KS>();
+  if (s8 <= 0 || s12 <= 0) return dq_v<D, 8, KS>(a);
   const long long t8 = (long long)a.BH * ((a.Nq + 255) / 256), t12 = (long long)a.BH * ((a.Nq + 383) / 384);
-  const double c8 = (double)((t8 + s8 - 1) / s8) * 8.0, c12 = (double)((t12 + s12 - 1) / s12) * 12.0 / 1.06;
-  return c12 < c8 ? dq_v<64, 12>(a) : dq_v<64, 8>(a);
+  const double c8 = (double)((t8 + s8 - 1) / s8) * 8.0, c12 = (double)((t12 + s12 - 1) / s12) * 12.0 / rate12;
+  return c12 < c8 ? dq_v<D, 12, KS>(a) : dq_v<D, 8, KS>(a);
 }
 
 hipError_t launch_bwd_dq(const BwdArgs& a) {
   if (a.ds != nullptr) return launch_bwd_dq_ds(a);
   switch (tile_width(a.d)) {
-    case 64: return dq_64(a);
-    case 96: return a.d <= 80 ? dq_v<96, 8, 5>(a) : dq_v<96, 8>(a);  // d <= 80: five contraction steps
+    case 64: return dq_8_or_12<64, 4>(a, 1.06);
+    case 96: return a.d <= 80 ? dq_8_or_12<96, 5>(a, 1.045) : dq_v<96, 8>(a);  // d <= 80: five contraction steps
     case 128: return dq_v<128, 8>(a);
     default: return dq_v<160, 8>(a);
   }

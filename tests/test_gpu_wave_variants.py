@@ -1,12 +1,14 @@
 """At the narrowest tile (head dims up to 64) the forward and dQ kernels
 choose between 8- and 12-wave workgroups from the grid size, and each dK/dV
-wave holds two 32-key blocks (256 keys per workgroup). B=1, H=6, N=22,001
-makes the six-head call take the 12-wave forward and dQ on a 256-CU part
-(two rounds of 384-query workgroups instead of three of 256) while each
-single-head call takes the 8-wave ones, and splits 4 of its 516 dK/dV key
-blocks where a single-head call splits all 86; every output must be bitwise
-equal between the two, and sampled query and key rows must match the fp64
-oracle."""
+wave holds two 32-key blocks (256 keys per workgroup); in the 96-wide tile
+with d <= 80 the dQ kernel makes the same choice and dK/dV runs six pairs of
+waves (192 keys). B=1, H=6, N=22,001 makes the six-head call take the
+12-wave dQ (and at d <= 64 forward) on a 256-CU part (two rounds of
+384-query workgroups instead of three of 256) while each single-head call
+takes the 8-wave ones; dK/dV splits 4 of its 516 key blocks at d <= 64 (none
+of 690 at d = 72) where a single-head call splits all 86 (115). Every
+output must be bitwise equal between the two, and sampled query and key
+rows must match the fp64 oracle."""
 import numpy as np
 import pytest
 
@@ -21,7 +23,7 @@ def np64(t):
     return t.detach().double().cpu().numpy()
 
 
-@pytest.mark.parametrize("d", [56, 64])
+@pytest.mark.parametrize("d", [56, 64, 72])
 def test_twelve_wave_grid_matches_single_heads_and_oracle(d):
     t = torch()
     B, H, N = 1, 6, 22001
