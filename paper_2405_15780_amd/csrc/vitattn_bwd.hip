@@ -2,13 +2,14 @@
 // backward, cited by the paper in Sec. II-F): P is recomputed from Q, K and
 // the saved logsumexp, never stored.
 //
-//   1. preprocess:  D_i = sum_c dO_ic O_ic                (HBM-bound)
-//   2. dK/dV kernel: one workgroup per 128 keys (256 at head dims up to 64;
-//      32 or 64 per wave, K and V held in registers); streams Q, dO, LSE and
-//      D in tiles of 64 queries:
+//   1. preprocess:  D_i = sum_c dO_ic O_ic    (HBM-bound; stored as -D_i)
+//   2. dK/dV kernel: one workgroup per 128 keys (in the recompute mode 256
+//      at head dims up to 64, 192 at head dims 65-80; 32 or 64 per wave, K
+//      and V held in registers); streams Q, dO, LSE and D in tiles of 64
+//      queries:
 //        S = Q K^T, P = exp2(S*scale*log2e - LSE*log2e)
 //        dV^T += dO^T P,  dP = dO V^T,  dS = P o (dP - D),  dK^T += Q^T dS
-//   3. dQ kernel: one workgroup per 256 queries (or 384 at head dims up to 64;
+//   3. dQ kernel: one workgroup per 256 queries (or 384 at head dims up to 80;
 //      32 per wave, Q and dO held in registers); streams K and V in tiles of
 //      32 keys:
 //        S^T = K Q^T, P^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T
