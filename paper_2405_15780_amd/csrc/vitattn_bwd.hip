@@ -415,6 +415,10 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
       constexpr int i = decltype(IC)::value;
       constexpr int a = i / KPW, kp = i % KPW;  // operand, key block
       constexpr int ph = phase_of(a), j = a - phase_start(ph), qb = ph & 1;
+      // the two phases that carry vector work run at a raised wave priority,
+      // so that their vector instructions issue ahead of the partner wave's
+      // matrix-core-only phases (measured 1.7-3.3 % faster, same bits)
+      if constexpr (j == 0 && kp == 0) __builtin_amdgcn_s_setprio(ph == 1 || ph == 2 ? 1 : 0);
       if constexpr (kp == 0 && a + AH < NA) aq[(a + AH) % (AH + 1)] = read_a(a + AH);
       if constexpr (ph < 2) {
         if constexpr (j == 0) {
@@ -436,6 +440,7 @@ __global__ __launch_bounds__(128 * KBW, KBW / 2) __attribute__((amdgpu_waves_per
       }
       sched_fence();
     });
+    __builtin_amdgcn_s_setprio(0);
     if constexpr (RP) {
 #pragma unroll
       for (int kp = 0; kp < KPW; ++kp)
@@ -767,6 +772,10 @@ __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu
       sched_fence();
       static_for<0, NOPS>([&](auto IC) __attribute__((always_inline)) {
         constexpr int i = decltype(IC)::value;
+        // the ops that carry vector work run at a raised wave priority
+        // (measured 0.3-1.1 % faster, same bits)
+        if constexpr (i == 0) __builtin_amdgcn_s_setprio(1);
+        if constexpr (i == W) __builtin_amdgcn_s_setprio(0);
         if constexpr (i + 1 < NOPS) aq[(i + 1) & 1] = load_op(i + 1);
         if constexpr (i < NS) {
           if constexpr (i % KS == 0) nxt[i / KS] = zero16();
