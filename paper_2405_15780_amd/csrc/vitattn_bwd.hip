@@ -773,8 +773,12 @@ __global__ __launch_bounds__(64 * NW, NW / 4) __attribute__((amdgpu_waves_per_eu
       static_for<0, NOPS>([&](auto IC) __attribute__((always_inline)) {
         constexpr int i = decltype(IC)::value;
         // the ops that carry vector work run at a raised wave priority
-        // (measured 0.3-1.1 % faster, same bits)
-        if constexpr (i == 0) __builtin_amdgcn_s_setprio(1);
+        // (measured 0.3-1.1 % faster, same bits); with three waves per SIMD
+        // the first half of the window runs one level higher still, so a
+        // wave early in its vector work goes ahead of one late in it (3 %
+        // faster at d=64, no change with two waves per SIMD)
+        if constexpr (i == 0) __builtin_amdgcn_s_setprio(NW > 8 ? 2 : 1);
+        if constexpr (NW > 8 && i == W / 2) __builtin_amdgcn_s_setprio(1);
         if constexpr (i == W) __builtin_amdgcn_s_setprio(0);
         if constexpr (i + 1 < NOPS) aq[(i + 1) & 1] = load_op(i + 1);
         if constexpr (i < NS) {
