@@ -75,7 +75,7 @@ def _identities(w, x, res):
     print(f"{w.name} identities", rep, flush=True)
     del f, g
     t.cuda.empty_cache()
-    # Sum identities: each dS_ij is rounded to bf16 (relative 2^-9) and D comes
+    # Sum identities: each dS_ij is rounded to bf16 (relative <= 2^-8) and D comes
     # from the fp32 O, so sum_j dS_ij = 0 holds to about 1e-3 of |dS|; a wrong
     # term would leave an O(1) residual. The inner-product identities use the
     # same dS on both sides and hold to fp32 rounding (calibrated on the 16,384-token workload:
@@ -208,7 +208,7 @@ def test_identical_keys_give_mean_of_v(d):
     lse = scale * np.einsum("bhnd,bhd->bhn", q, k[:, :, 0]) + np.log(N)
     np.testing.assert_allclose(got["lse"], lse, atol=1e-4)
     # dQ_i = s k sum_j dS_ij and each row of dS sums to zero; the kernels round
-    # dS to bf16 (relative 2^-9), so dQ_i stays below 1e-2 of the scale
+    # dS to bf16 (relative <= 2^-8), so dQ_i stays below 1e-2 of the scale
     # s |k| ||dS_i|| it would have without that cancellation
     dout, vbar = oracle.decode_bf16(x["dout"]), v.mean(axis=2, keepdims=True)
     ds = np.einsum("bhic,bhjc->bhij", dout, v - vbar) / N
