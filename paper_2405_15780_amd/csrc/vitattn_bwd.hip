@@ -15,13 +15,14 @@
 //        S^T = K Q^T, P^T, dP^T = V dO^T, dS^T, dQ^T += K^T dS^T
 // Splitting dQ from dK/dV costs one extra recomputation of S and dP but needs
 // no atomics for dQ (accumulating dQ inside the dK/dV pass would add a 4-byte
-// atomic per query, key block and column, B H N^2 d / 32 of them, and fp32
-// atomics sustain only ~1.3 TB/s on this part). The only atomics are those of
-// the dK/dV kernel's split key blocks (two fp32 adds onto zero per element,
-// which commute exactly, and every whole block forms the same two rounded
-// partial sums), so results are deterministic and independent of the grid. As in the forward pass, operands
-// may have any batch / head / row strides, and a head dim d below the tile
-// width D is padded with zero columns on load and cut off on store.
+// atomic per query, column and 128-key workgroup, B H N^2 d / 128 of them,
+// and fp32 atomics sustain only ~1.3 TB/s on this part). The only atomics are
+// those of the dK/dV kernel's split key blocks (two fp32 adds onto zero per
+// element, which commute exactly, and every whole block forms the same two
+// rounded partial sums), so results are deterministic and independent of the
+// grid. As in the forward pass, operands may have any batch / head / row
+// strides, and a head dim d below the tile width D is padded with zero
+// columns on load and cut off on store.
 #include <atomic>
 #include <type_traits>
 
@@ -81,7 +82,8 @@ __device__ __forceinline__ void stats_dma(rsrc_t rd, rsrc_t rl, int row0, float*
 
 // One workgroup = 2*KBW waves = 32*KBW*KPW keys of one (b, h): KBW pairs of
 // waves, each pair owning KPW blocks of 32 keys (KBW = 4, KPW = 1: 8 waves,
-// 128 keys; KBW = 4, KPW = 2 at the narrowest tile: 8 waves, 256 keys). The
+// 128 keys; KBW = 4, KPW = 2 at the narrowest tile: 8 waves, 256 keys;
+// KBW = 6, KPW = 1 in the 96-wide tile at d <= 80: 12 waves, 192 keys). The
 // two waves of a pair split the roles (waves share the SIMDs round robin, so
 // the vector and matrix phases of the roles interleave):
 //   role P  (waves 0 .. KBW-1): holds K, accumulates dV^T.
@@ -1223,10 +1225,11 @@ static int dq_resident_workgroups() {
   return n > 0 ? n : 0;
 }
 
-// At the narrowest tile (168 VGPRs) and at D = 96 with five contraction
-// steps (168, one 16-byte operand spilled and reloaded three times per six
-// tiles) the dQ kernel fits three waves per SIMD: 12 waves (384 queries) per workgroup share each K /
-// V tile, faster per query than 8 waves (~6 % at D = 64, B=4, H=1, N=188,416;
+// At the narrowest tile (168 VGPRs, three values spilled and reloaded only
+// after the tile loop) and at D = 96 with five contraction steps (168, one
+// 16-byte operand spilled and reloaded three times per six tiles) the dQ
+// kernel fits three waves per SIMD: 12 waves (384 queries) per workgroup share
+// each K / V tile, faster per query than 8 waves (~6 % at D = 64, B=4, H=1, N=188,416;
 // ~4.5 % at d = 72, B=1, H=2-3, N=50,001-188,416), but in coarser work items.
 // The variant with the shorter estimated time (whole rounds of resident
 // workgroups x queries per workgroup / that rate) is launched; both compute
