@@ -50,9 +50,11 @@
  *    zero give the same bits in either order. Every key block, split or
  *    not, sums its query tiles as the same two rounded partial sums (split
  *    at the middle query tile) and adds them, so splitting changes no bit.
- *    Which blocks split depends on the number of key blocks (B*H*ceil(N/128))
- *    and the device's CU count, looked up once per device at the first
- *    backward call (no stream work, so a graph capture may hold it).
+ *    Which blocks split depends on the number of key-block workgroups
+ *    (B*H*ceil(N/K), K = 128 keys, or in the default mode 256 at head dims up
+ *    to 64 and 192 at 65-80) and the device's CU count, looked up once per
+ *    device at the first backward call (no stream work, so a graph capture
+ *    may hold it).
  *  - Calls are thread-safe; concurrent calls on different streams are fine.
  */
 #ifndef VITATTN_H
@@ -134,8 +136,8 @@ int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout
  * Attention over one segment of the keys, and the merge of such partial
  * results. Sequence parallelism over contiguous segments (Long Sequence
  * Segmentation, paper Sec. I and II "Sequence Parallel"; one segment per
- * worker) hands one GPU its queries and the keys of one segment at a time. Softmax over a union of key sets factors
- * over the sets:
+ * worker) hands one GPU its queries and the keys of one segment at a time.
+ * Softmax over a union of key sets factors over the sets:
  *
  *     LSE_i = log sum_s exp(LSE_s,i),   O_i = sum_s exp(LSE_s,i - LSE_i) O_s,i
  *
