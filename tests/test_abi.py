@@ -327,6 +327,7 @@ def fwd_strided(b, sq=None, sk=None, sv=None, so=None, B=2, H=2, Nq=8, Nk=8, d=7
     (dict(so=S(1152, 72, 72)), E_INVAL),              # output heads overlap rows
     (dict(so=S(0, 576, 72)), E_INVAL),                # output batches repeat
     (dict(sq=S(0, 0, 1 << 27)), E_INVAL),             # (rows + 256) * row bytes past 2^31
+    (dict(sk=S(0, 0, 131064), Nk=7937), E_INVAL),     # the same, one legal pitch past the largest (131,056)
     (dict(d=100), E_UNSUP), (dict(d=168), E_UNSUP), (dict(B=0), E_INVAL), (dict(scale=0.0), E_INVAL),
 ])
 def test_fwd_strided_rejects_bad_layouts(kw, expected):

@@ -194,3 +194,79 @@ def test_paper_head_dims_at_16k_tokens(d, H):
     ref = oracle.forward_backward(x["q"], x["k"], x["v"], x["dout"], scale, heads=[(0, 0)])
     got = {n: np64(v[0, 0]) for n, v in res.items()}
     assert_close(got, {n: a[0, 0] for n, a in ref.items()}, label=f"N={N} d={d} head (0,0)")
+
+
+def _pitched_input(bits, pitch):
+    """bf16 bits [1, 1, N, d] placed in rows `pitch` elements apart, NaN
+    between them (a read of it would poison the outputs); returns the
+    [1, 1, N, d] view."""
+    t = torch()
+    N, d = bits.shape[2], bits.shape[3]
+    buf = t.full((N, pitch), float("nan"), dtype=t.bfloat16, device="cuda")
+    buf[:, :d] = to_device(bits)[0, 0]
+    return buf[:, :d][None, None]
+
+
+def test_largest_input_pitch_and_outputs_past_4_gib():
+    """Input rows as far apart as the library allows ((N + 256) * row * 2 bytes
+    just below 2^31: the kernels address one head's rows with 32-bit offsets)
+    and fp32 output rows spanning more than 2^32 bytes (64-bit offsets): every
+    output bitwise equal to the dense call's, nothing written between the
+    output rows, and all five outputs against the oracle element by element."""
+    t = torch()
+    B, H, N, d = 1, 1, 7937, 8
+    pitch_in, pitch_out = 131056, 135304
+    assert (N + 256) * pitch_in * 2 < 2**31 <= (N + 256) * (pitch_in + 8) * 2
+    assert N * pitch_out * 4 > 2**32
+    print(f"case largest pitch N={N} d={d} in={pitch_in} out={pitch_out}", flush=True)
+    x = workloads.make_small_inputs(B, H, N, d, seed=1900)
+    scale = 1.0 / np.sqrt(d)
+    ins = [_pitched_input(x[n], pitch_in) for n in ("q", "k", "v", "dout")]
+    sentinel = 12345.0
+    bufs = [t.full((N, pitch_out), sentinel, dtype=t.float32, device="cuda") for _ in range(4)]  # o dq dk dv
+    outs = (bufs[0][:, :d][None, None], t.empty((B, H, N), dtype=t.float32, device="cuda"),
+            *(b[:, :d][None, None] for b in bufs[1:]))
+    res = run(*ins, scale, outs=outs)
+    dense = dense_run(x, scale)
+    for n in res:
+        assert t.equal(res[n], dense[n]), f"{n} differs bitwise from the dense layout"
+    for name, b in zip(("o", "dq", "dk", "dv"), bufs):
+        assert int(t.count_nonzero(b != sentinel)) == N * d, f"{name}: a write missed its row or left it"
+    got = {n: np64(v) for n, v in res.items()}
+    del ins, bufs, outs, res
+    t.cuda.empty_cache()
+    assert_close(got, oracle.forward_backward(x["q"], x["k"], x["v"], x["dout"], scale), label="largest pitch")
+
+
+def test_longest_sequence_at_a_16_kib_pitch():
+    """N = 130,815 input rows 16 KB apart, the longest sequence the 32-bit
+    offsets allow at that pitch, with ragged last tiles: bitwise equal to the
+    dense call; sampled query rows (O, LSE, dQ) against the oracle; dK and dV
+    through identities that hold at any size (dS rows sum to zero, so the
+    dK rows sum to zero; P rows sum to one, so the dV rows sum to the dO
+    rows' sum)."""
+    t = torch()
+    B, H, N, d, pitch = 1, 1, 130815, 8, 8192
+    assert (N + 256) * pitch * 2 < 2**31 <= (N + 257) * pitch * 2
+    print(f"case longest sequence N={N} d={d} pitch={pitch}", flush=True)
+    x = workloads.make_small_inputs(B, H, N, d, seed=1901)
+    scale = 1.0 / np.sqrt(d)
+    ins = [_pitched_input(x[n], pitch) for n in ("q", "k", "v", "dout")]
+    res = run(*ins, scale)
+    del ins
+    t.cuda.empty_cache()
+    dense = dense_run(x, scale)
+    for n in res:
+        assert t.equal(res[n], dense[n]), f"{n} differs bitwise from the dense layout"
+    rng = np.random.default_rng(1901)
+    idx = np.unique(np.concatenate([[0, N - 1], rng.choice(N, 62, replace=False)]))
+    rows = np.stack([np.zeros_like(idx), np.zeros_like(idx), idx], axis=1)
+    ref = oracle.query_rows(x["q"], x["k"], x["v"], scale, rows, dout=x["dout"])
+    sel = tuple(t.from_numpy(rows[:, i]).cuda() for i in range(3))
+    assert_close({n: np64(res[n][sel]) for n in ("o", "lse", "dq")}, ref, names=("o", "lse", "dq"),
+                 label="longest sequence sampled query rows")
+    dk, dv, g = res["dk"][0, 0].double(), res["dv"][0, 0].double(), to_device(x["dout"])[0, 0].double()
+    r_dk = (dk.sum(0).norm() / dk.norm()).item()
+    r_dv = ((dv.sum(0) - g.sum(0)).norm() / dv.norm()).item()
+    print("longest sequence identities", {"sum_dk": r_dk, "sum_dv": r_dv}, flush=True)
+    assert r_dk < 1e-2 and r_dv < 1e-2
