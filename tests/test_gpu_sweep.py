@@ -1,6 +1,7 @@
 """Seeded random sweep of valid attention calls: batch, heads, query and key
-counts (Nq != Nk), every head dim up to 160, dense / sequence-major / padded
-operand layouts and both backward modes, each compared element by element
+counts (Nq != Nk), every head dim up to 160, softmax scales of 1/2, 1 and 2
+times 1/sqrt(d), dense / sequence-major / padded operand layouts and both
+backward modes, each compared element by element
 with the oracle (forward, and the backward of one key segment holding all
 keys)."""
 import numpy as np
@@ -22,7 +23,7 @@ def draw_case(rng):
     return dict(B=int(rng.choice([1, 2, 3])), H=int(rng.choice([1, 2, 3, 5])), Nq=int(rng.integers(1, 600)),
                 Nk=int(rng.integers(1, 600)), d=int(rng.choice(np.arange(8, 161, 8))),
                 layout=str(rng.choice(["dense", "bnhd", "padded"])), store_ds=bool(rng.integers(0, 2)),
-                pad=8 * int(rng.integers(1, 5)))
+                pad=8 * int(rng.integers(1, 5)), scale_x=float(rng.choice([0.5, 1.0, 2.0])))
 
 
 @pytest.mark.parametrize("seed", [1, 2, 3])
@@ -38,7 +39,7 @@ def test_random_valid_calls_match_the_oracle(seed):
         print(label, flush=True)
         xq = workloads.make_small_inputs(B, H, Nq, d, seed=100000 * seed + 2 * case)
         xk = workloads.make_small_inputs(B, H, Nk, d, seed=100000 * seed + 2 * case + 1, with_dout=False)
-        scale = 1.0 / np.sqrt(d)
+        scale = c["scale_x"] / np.sqrt(d)
 
         def put(bits):
             if layout == "dense":
