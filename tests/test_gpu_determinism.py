@@ -4,7 +4,8 @@ stores, dQ from the stored blocks), dQ accumulated over key segments, the
 merge, and the channel aggregation with its dq partials. The only atomics
 are the dK/dV kernel's split key blocks (all of this shape's key blocks: two
 fp32 adds onto zero per element, which commute exactly), so two runs on the
-same inputs must agree bit for bit."""
+same inputs must agree bit for bit. Calls made at the same time from two
+host threads on two streams give the bits of the same calls made alone."""
 import numpy as np
 import pytest
 
@@ -49,3 +50,52 @@ def test_repeated_runs_are_bitwise_equal():
     for name, tensors in first.items():
         for i, (a, b) in enumerate(zip(tensors, second[name])):
             assert t.equal(a, b), f"{name} output {i} differs between two runs"
+
+
+def test_concurrent_calls_on_two_streams_from_two_threads():
+    """Two host threads, each on a stream of its own (default priority), run
+    forward and backward passes of different shapes and head dims at the same
+    time, three times each, on the first calls of their kernel variants in
+    this process where the test runs alone: every output is bitwise equal to
+    that of the same call made on its own. The calls share nothing but the
+    per-device kernel lookups (atomics), so they must not interfere."""
+    import threading
+
+    import paper_2405_15780_amd as va
+
+    t = torch()
+    cases = [(1, 3, 3001, 56), (2, 1, 2500, 136)]
+    print(f"case concurrent streams {cases}", flush=True)
+    inputs = [{n: to_device(a) for n, a in workloads.make_small_inputs(*c, seed=9700 + i).items()}
+              for i, c in enumerate(cases)]
+    t.cuda.synchronize()
+
+    def call(x):
+        o, lse = va.fwd(x["q"], x["k"], x["v"])
+        return (o, lse) + tuple(va.bwd(x["q"], x["k"], x["v"], o, lse, x["dout"]))
+
+    results = [[None] * 3 for _ in cases]
+    errors = []
+
+    def worker(i):
+        try:
+            s = t.cuda.Stream()
+            with t.cuda.stream(s):
+                for rep in range(3):
+                    results[i][rep] = call(inputs[i])
+            s.synchronize()
+        except Exception as e:  # reported on the main thread
+            errors.append((i, e))
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(len(cases))]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors
+    alone = [call(x) for x in inputs]
+    t.cuda.synchronize()
+    for i, c in enumerate(cases):
+        for rep in range(3):
+            for n, a, b in zip(("o", "lse", "dq", "dk", "dv"), results[i][rep], alone[i]):
+                assert t.equal(a, b), f"{c} repeat {rep}: {n} differs from the call made alone"
