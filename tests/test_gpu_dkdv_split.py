@@ -5,13 +5,15 @@ into zeroed rows, while whole key blocks form the same two partial sums
 (the first stored at the midpoint), so the bits do not depend on the
 split. The shapes below put whole and split key blocks in one
 launch on a 256-CU part with one dK/dV workgroup per CU (B*H*ceil(N/BK)
-work items, BK = 128 keys, or 256 at head dims up to 64 in the recompute
-mode: 257 -> 256 whole + 1 split, 600 -> 512 + 88, 280 -> 256 + 24, 260 ->
-256 + 4 with 130 query tiles per half, the last one ragged, and in the last
-work item a wave whose first 32-key block holds 24 keys and whose second
-lies past the end), including an odd tile count (the second half one tile
-longer). Both backward modes, against the fp64 oracle;
-on any other device the same comparisons hold whatever the split."""
+work items, BK = 128 keys, or in the recompute mode 256 at head dims up to
+64 and 192 at 65-80: 257 -> 256 whole + 1 split, 600 -> 512 + 88, 280 ->
+256 + 24, 260 -> 256 + 4 with 130 query tiles per half, the last one
+ragged, and in the last work item a wave whose first 32-key block holds 24
+keys and whose second lies past the end; at d = 72, 270 -> 256 + 14 twelve-
+wave work items in the recompute mode and 360 -> 256 + 104 in the dS mode),
+including an odd tile count (the second half one tile longer). Both
+backward modes, against the fp64 oracle; on any other device the same
+comparisons hold whatever the split."""
 import numpy as np
 import pytest
 
@@ -21,7 +23,8 @@ from gpu_util import assert_close, run_hip, torch
 
 pytestmark = pytest.mark.gpu
 
-CASES = [(1, 257, 256, 64), (1, 300, 130, 128), (2, 70, 200, 160), (1, 4, 16600, 64), (1, 33, 1000, 96)]
+CASES = [(1, 257, 256, 64), (1, 300, 130, 128), (2, 70, 200, 160), (1, 4, 16600, 64), (1, 33, 1000, 96),
+         (1, 45, 1000, 72)]
 
 
 def np64(t):
@@ -71,7 +74,8 @@ def test_head_alone_and_among_others(store_ds):
         assert t.equal(full[name][:, 2:3], alone[name]), name
 
 
-@pytest.mark.parametrize("B,H,N,d", [(1, 300, 130, 128), (1, 4, 16600, 64), (1, 33, 1000, 96), (2, 70, 200, 160)])
+@pytest.mark.parametrize("B,H,N,d", [(1, 300, 130, 128), (1, 4, 16600, 64), (1, 33, 1000, 96), (2, 70, 200, 160),
+                                     (1, 45, 1000, 72)])
 def test_split_blocks_bitwise_equal_to_single_head_calls(B, H, N, d):
     # every head of a launch whose last round splits (see CASES) against the
     # same head in a call of its own, where the grid is far from a whole
