@@ -34,6 +34,12 @@
  *    costs what d = 96 costs. Any N >= 1 with (N + 256) * row_stride * 2 below
  *    2^31 for every bf16 operand (the kernels address one head's rows with
  *    32-bit offsets; N up to 8,388,351 for dense d = 128) and B*H*N below 2^31.
+ *    Every kernel launch must also stay below 2^32 work-items: 2*B*H*(N + 383)
+ *    for the forward; for the backward and its stages also
+ *    4*B*H*(N + 191) + 2^19 and B*H*N times 8, 16 or 32 (head dims up to 64,
+ *    128, 160); B*H*N*d/4 + 256 for the merge. These bind only at head dims
+ *    of 16 or less (wider rows run out of memory first); a call past them
+ *    returns VITATTN_E_INVAL.
  *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *    the call returns without waiting. Execution faults surface at the
  *    caller's next synchronisation on that stream.
@@ -279,7 +285,8 @@ int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, flo
  * y is the contiguous [B][Hl][N][row] input (or output) of the attention
  * entry points. The collective itself is not part of this library.
  *   B, Nl, H, P: >= 1 with H divisible by P, B <= 65535, Nl*row_bytes/16 < 2^31
- *                and ceil(Nl*row_bytes/4096)*H < 2^31.
+ *                and ceil(Nl*row_bytes/4096)*H < 2^24 (256 work-items per
+ *                block, below 2^32 per launch).
  *   row_bytes  : a multiple of 16, >= 16.
  *   src, dst   : device pointers, 16-byte aligned, not overlapping
  *                (src == dst is rejected; partial overlap is not detected).
@@ -306,7 +313,8 @@ int vitattn_ulysses_unpack_out(const void* recv, void* x, int B, int Nl, int H, 
  *
  * Layouts (row-major): q bf16 [H][d]; k, v bf16 [M][H][C][d]; o fp32
  * [M][H][d]; lse fp32 [M][H]; dout bf16 [M][H][d]; dq fp32 [H][d]; dk, dv
- * fp32 [M][H][C][d]. M, H, C >= 1 (any C; the paper's case is C = 92);
+ * fp32 [M][H][C][d]. M, H, C >= 1 (any C; the paper's case is C = 92) with
+ * (M + 3)*H and H*d below 2^26 (64 work-items each per launch, below 2^32);
  * d in {64, 128}; scale finite and > 0. Bound by HBM bandwidth. dq is
  * reduced in a fixed order (no atomics): results are bitwise reproducible.
  */

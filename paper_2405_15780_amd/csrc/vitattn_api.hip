@@ -38,6 +38,24 @@ int check_sizes(int B, int H, int N, int d) {
 
 bool scale_ok(float s) { return isfinite(s) && s > 0.f; }
 
+// Every launch must stay below 2^32 work-items (a dispatch's grid size is
+// 32-bit; a larger one would fail at launch, after the call's earlier
+// kernels had run). The forward and dQ kernels run 2 per query row plus the
+// padding of each head's last workgroup (up to 383 rows), the dK/dV kernel
+// up to 4 per key row plus its padding (up to 191 rows per head) and the
+// split workgroups of at most half a round (one per CU, 768 work-items
+// each), the row-dot pass 8, 16 or 32 per row (head dims up to 64, 128,
+// 160) and the merge d/4 per row. These bounds bind only at head dims of 16
+// or less; wider rows run out of memory first.
+constexpr long long kMaxWorkItems = 1LL << 32;
+bool fwd_items_ok(int B, int H, int Nq) { return 2LL * B * H * (Nq + 383LL) < kMaxWorkItems; }
+bool bwd_items_ok(int B, int H, int Nq, int Nk, int d) {
+  const long long bh = (long long)B * H, lpr = d <= 64 ? 8 : d <= 128 ? 16 : 32;
+  return fwd_items_ok(B, H, Nq) && 4 * bh * (Nk + 191LL) + (1LL << 19) < kMaxWorkItems &&
+         bh * Nq * lpr + 256 < kMaxWorkItems;
+}
+bool merge_items_ok(int B, int H, int N, int d) { return (long long)B * H * N * (d / 4) + 256 < kMaxWorkItems; }
+
 // key rows obey the same limits as query rows
 int check_sizes_kv(int B, int H, int Nq, int Nk, int d) {
   const int st = check_sizes(B, H, Nq, d);
@@ -144,6 +162,7 @@ int vitattn_fwd_strided(const void* q, vitattn_strides sq, const void* k, vitatt
   try {
     int st = check_sizes_kv(B, H, Nq, Nk, d);
     if (st != VITATTN_OK) return st;
+    if (!fwd_items_ok(B, H, Nq)) return VITATTN_E_INVAL;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
       return VITATTN_E_INVAL;
     if (!scale_ok(scale)) return VITATTN_E_INVAL;
@@ -233,6 +252,7 @@ int vitattn_bwd_strided(const void* q, vitattn_strides sq, const void* k, vitatt
   try {
     int st = check_sizes_kv(B, H, Nq, Nk, d);
     if (st != VITATTN_OK) return st;
+    if (!bwd_items_ok(B, H, Nq, Nk, d)) return VITATTN_E_INVAL;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(lse) ||
         !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
       return VITATTN_E_INVAL;
@@ -270,6 +290,7 @@ int vitattn_merge(const float* o_parts, const float* lse_parts, int n_parts, flo
   try {
     int st = check_sizes(B, H, N, d);  // d: a multiple of 8 up to 160, as for the attention
     if (st != VITATTN_OK) return st;
+    if (!merge_items_ok(B, H, N, d)) return VITATTN_E_INVAL;
     if (n_parts < 1 || n_parts > VITATTN_MERGE_MAX_PARTS) return VITATTN_E_INVAL;
     if (!aligned16(o_parts) || !aligned16(lse_parts) || !aligned16(o) || !aligned16(lse)) return VITATTN_E_INVAL;
     vitattn::MergeArgs a;
@@ -293,6 +314,7 @@ int vitattn_bwd_rowdot(const float* o, const void* dout, const float* lse, int B
   try {
     int st = check_sizes(B, H, N, d);
     if (st != VITATTN_OK) return st;
+    if (!bwd_items_ok(B, H, N, N, d)) return VITATTN_E_INVAL;
     if (!aligned16(o) || !aligned16(dout) || !aligned16(lse)) return VITATTN_E_INVAL;
     st = check_workspace(workspace, workspace_bytes, B, H, N, d);
     if (st != VITATTN_OK) return st;
@@ -310,6 +332,7 @@ int vitattn_bwd_dkdv(const void* q, const void* k, const void* v, const void* do
   try {
     int st = check_sizes(B, H, N, d);
     if (st != VITATTN_OK) return st;
+    if (!bwd_items_ok(B, H, N, N, d)) return VITATTN_E_INVAL;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(lse) || !aligned16(dk) ||
         !aligned16(dv))
       return VITATTN_E_INVAL;
@@ -330,6 +353,7 @@ int vitattn_bwd_dq(const void* q, const void* k, const void* v, const void* dout
   try {
     int st = check_sizes(B, H, N, d);
     if (st != VITATTN_OK) return st;
+    if (!bwd_items_ok(B, H, N, N, d)) return VITATTN_E_INVAL;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(lse) || !aligned16(dq))
       return VITATTN_E_INVAL;
     if (!scale_ok(scale)) return VITATTN_E_INVAL;
@@ -350,7 +374,7 @@ static int ulysses(const void* src, void* dst, int B, int Nl, int H, int P, int 
     if (!aligned16(src) || !aligned16(dst) || src == dst) return VITATTN_E_INVAL;
     // grid limits: B indexes grid.y, (token tiles x H) grid.x, Nl*row_bytes/16 a 32-bit thread index
     if (B > 65535 || (long long)Nl * (row_bytes / 16) > 0x7fffffffLL) return VITATTN_E_INVAL;
-    if (vitattn::ulysses_blocks(Nl, H, row_bytes) > 0x7fffffffL) return VITATTN_E_INVAL;
+    if (vitattn::ulysses_blocks(Nl, H, row_bytes) * 256 >= kMaxWorkItems) return VITATTN_E_INVAL;  // 256 per block
     if ((double)B * Nl * H * row_bytes > 9.0e18) return VITATTN_E_INVAL;
     vitattn::UlyssesArgs a;
     a.src = src;
@@ -389,6 +413,9 @@ static int check_agg(int M, int H, int C, int d, float scale) {
   if (M < 1 || H < 1 || C < 1) return VITATTN_E_INVAL;
   if (d != 64 && d != 128) return VITATTN_E_UNSUPPORTED;
   if ((long long)M * H > 0x7fffffffLL || (long long)H * d > 0x7fffffffLL) return VITATTN_E_INVAL;
+  // launches below 2^32 work-items: 64 per (patch, head) in the forward and
+  // backward (patches in groups of four), 64 per dq column in its reduction
+  if ((M + 3LL) * H * 64 >= kMaxWorkItems || ((long long)H * d + 15) * 64 >= kMaxWorkItems) return VITATTN_E_INVAL;
   if ((double)M * H * C * d > 4.0e18) return VITATTN_E_INVAL;
   return scale_ok(scale) ? VITATTN_OK : VITATTN_E_INVAL;
 }
@@ -503,6 +530,7 @@ int vitattn_bwd_noalloc(const void* q, const void* k, const void* v, const float
   try {
     int st = check_sizes(B, H, N, d);
     if (st != VITATTN_OK) return st;
+    if (!bwd_items_ok(B, H, N, N, d)) return VITATTN_E_INVAL;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(lse) ||
         !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
       return VITATTN_E_INVAL;
@@ -526,6 +554,7 @@ int vitattn_bwd_dkdv_ds(const void* q, const void* k, const void* v, const void*
   try {
     int st = check_sizes(B, H, N, d);
     if (st != VITATTN_OK) return st;
+    if (!bwd_items_ok(B, H, N, N, d)) return VITATTN_E_INVAL;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) || !aligned16(lse) || !aligned16(dk) ||
         !aligned16(dv))
       return VITATTN_E_INVAL;
@@ -547,6 +576,7 @@ int vitattn_bwd_dq_from_ds(const void* k, float* dq, int B, int H, int N, int d,
   try {
     int st = check_sizes(B, H, N, d);
     if (st != VITATTN_OK) return st;
+    if (!bwd_items_ok(B, H, N, N, d)) return VITATTN_E_INVAL;
     if (!aligned16(k) || !aligned16(dq)) return VITATTN_E_INVAL;
     if (!scale_ok(scale) || !ds_mode_ok(N)) return VITATTN_E_INVAL;
     if (workspace == nullptr || !aligned16(workspace) ||

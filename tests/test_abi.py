@@ -88,6 +88,8 @@ def fwd(b, B=1, H=1, N=8, d=64, scale=0.125, override=None):
     (dict(d=256), E_UNSUP),
     (dict(scale=float("nan")), E_INVAL), (dict(scale=float("inf")), E_INVAL), (dict(scale=0.0), E_INVAL),
     (dict(scale=-0.125), E_INVAL), (dict(B=65536, H=65536, N=2), E_INVAL),
+    # B*H*N below 2^31 but 2*B*H*(N + 383) work-items past 2^32
+    (dict(B=2, H=2_800_000, N=1, d=8), E_INVAL),
 ])
 def test_fwd_rejects_bad_sizes_and_scale(kw, expected):
     b = Bufs()
@@ -121,6 +123,10 @@ def bwd(b, B=1, H=1, N=8, d=64, scale=0.125, ws_bytes=None, override=None):
     (dict(N=0), E_INVAL), (dict(d=84), E_UNSUP), (dict(scale=float("nan")), E_INVAL),
     (dict(ws_bytes=31), E_WS), (dict(ws_bytes=0), E_WS), (dict(override={9: None}), E_WS),
     (dict(override={9: 12345}), E_WS),
+    # launches past 2^32 work-items: the row-dot pass (8 per row at d = 8)
+    # and the dK/dV kernel (4 per key row plus padding), with B*H*N < 2^31
+    (dict(B=8, H=8, N=1 << 23, d=8, ws_bytes=1 << 40), E_INVAL),
+    (dict(B=4, H=1_125_000, N=64, d=8, ws_bytes=1 << 40), E_INVAL),
 ])
 def test_bwd_rejects_bad_arguments(kw, expected):
     b = Bufs()
@@ -224,6 +230,7 @@ def test_bwd_kv_workspace_is_sized_by_query_rows():
     (dict(P=0), E_INVAL), (dict(P=-3), E_INVAL), (dict(P=65537), E_INVAL), (dict(N=0), E_INVAL),
     (dict(d=100), E_UNSUP), (dict(d=168), E_UNSUP), (dict(d=0), E_UNSUP), (dict(override={0: None}), E_INVAL),
     (dict(override={3: 4104}), E_INVAL),
+    (dict(H=128, N=1 << 20, d=160), E_INVAL),  # B*H*N*d/4 work-items past 2^32
 ])
 def test_merge_rejects_bad_arguments(kw, expected):
     b = Bufs()
@@ -242,7 +249,8 @@ def test_merge_rejects_bad_arguments(kw, expected):
 @pytest.mark.parametrize("kw", [dict(H=6, P=4), dict(P=0), dict(B=0), dict(Nl=0), dict(row_bytes=24),
                                 dict(row_bytes=0), dict(src=None), dict(dst=None), dict(src="dst"),
                                 dict(src=4100), dict(B=70000, P=2, H=2),
-                                dict(Nl=1 << 24, H=1 << 16, P=1, row_bytes=16)])
+                                dict(Nl=1 << 24, H=1 << 16, P=1, row_bytes=16),
+                                dict(Nl=1 << 20, H=64, P=1, row_bytes=1024)])  # 2^24 blocks of 256: 2^32 items
 def test_ulysses_layouts_reject_bad_arguments(name, kw):
     b = Bufs()
     args = dict(src=b.p(0), dst=b.p(1), B=1, Nl=4, H=4, P=2, row_bytes=32)
@@ -257,6 +265,7 @@ def test_ulysses_layouts_reject_bad_arguments(name, kw):
 @pytest.mark.parametrize("kw,expected", [
     (dict(M=0), E_INVAL), (dict(H=0), E_INVAL), (dict(C=0), E_INVAL), (dict(d=72), E_UNSUP),
     (dict(scale=float("inf")), E_INVAL), (dict(scale=-1.0), E_INVAL), (dict(M=70000, H=70000), E_INVAL),
+    (dict(M=1 << 24, H=4), E_INVAL),  # (M + 3) * H * 64 work-items past 2^32
     (dict(override={0: None}), E_INVAL), (dict(override={3: 4100}), E_INVAL),
 ])
 def test_agg_fwd_rejects_bad_arguments(kw, expected):
