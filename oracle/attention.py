@@ -168,7 +168,7 @@ def row_statistics(q, k, v, dout, scale, b, h, block=QUERY_BLOCK):
     forward pass of that head. These are what a key row's dK and dV need."""
     s = fp32_scale(scale)
     K, V = _as_f64(k[b, h]), _as_f64(v[b, h])
-    N = K.shape[0]
+    N = q.shape[2]  # query rows (the keys may be a different number)
     lse = np.empty(N)
     D = np.empty(N)
     for r0 in range(0, N, block):

@@ -282,6 +282,29 @@ def test_query_rows_and_key_rows_match_full_pass():
     np.testing.assert_allclose(dv, full["dv"][1, 0, keys], rtol=1e-11, atol=1e-13)
 
 
+@pytest.mark.parametrize("Nq,Nk", [(37, 90), (90, 37)])
+def test_row_statistics_and_key_rows_with_other_key_counts(Nq, Nk):
+    # queries and keys of different lengths: LSE and D for every query row,
+    # and dK, dV of sampled keys, against the forward and the segment backward
+    from oracle.segments import segment_backward
+
+    rng = np.random.default_rng(16)
+    q, dout = (workloads.random_bf16(rng, (1, 2, Nq, 8)) for _ in range(2))
+    k, v = (workloads.random_bf16(rng, (1, 2, Nk, 8)) for _ in range(2))
+    s = 0.4
+    o, lse_f = oracle.forward(q, k, v, s)
+    lse, D = oracle.row_statistics(q, k, v, dout, s, 0, 1)
+    assert lse.shape == (Nq,) and D.shape == (Nq,)
+    np.testing.assert_allclose(lse, lse_f[0, 1], rtol=1e-14)
+    np.testing.assert_allclose(D, np.einsum("ic,ic->i", oracle.decode_bf16(dout)[0, 1], o[0, 1]), rtol=1e-12,
+                               atol=1e-14)
+    keys = np.array([0, 11, Nk - 1])
+    dk, dv = oracle.key_rows(q, k, v, dout, s, 0, 1, keys, lse, D, block=16)
+    _, dk_full, dv_full = segment_backward(q, k, v, dout, o, lse_f, s)
+    np.testing.assert_allclose(dk, dk_full[0, 1, keys], rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(dv, dv_full[0, 1, keys], rtol=1e-11, atol=1e-13)
+
+
 def test_row_ranges_sum_to_full_pass():
     rng = np.random.default_rng(15)
     bits = {n: workloads.random_bf16(rng, (1, 2, 90, 8)) for n in ("q", "k", "v", "dout")}
