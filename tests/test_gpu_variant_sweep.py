@@ -4,7 +4,9 @@ d <= 64, 12-wave dK/dV and five contraction steps at d <= 80, six at 88-96),
 dense or sequence-major, Nq != Nk. Each launch must give the same bits as
 single-head calls of two of its heads (which take other variants and other
 dK/dV splits), dK and dV must be bitwise equal between the two backward
-modes, and sampled query rows must match the fp64 oracle."""
+modes, and sampled query rows (O, LSE, dQ) and, where one head's oracle pass
+costs at most 1.5e8 scores, sampled key rows (dK, dV) must match the fp64
+oracle."""
 import numpy as np
 import pytest
 
@@ -76,3 +78,13 @@ def test_variant_grids_match_single_heads_modes_and_oracle(seed):
             else:
                 rel = np.linalg.norm(g64 - r) / np.linalg.norm(r)
                 assert rel <= 1e-2, (name, rel)
+        if Nq * Nk <= 1.5e8:
+            b, h = int(rng.integers(0, B)), int(rng.integers(0, H))
+            lse_r, D_r = oracle.row_statistics(xq["q"], xk["k"], xk["v"], xq["dout"], scale, b, h)
+            keys = np.sort(rng.choice(Nk, min(16, Nk), replace=False))
+            rdk, rdv = oracle.key_rows(xq["q"], xk["k"], xk["v"], xq["dout"], scale, b, h, keys, lse_r, D_r)
+            kk = t.from_numpy(keys).cuda()
+            for name, got, r in (("dk", dk, rdk), ("dv", dv, rdv)):
+                rel = np.linalg.norm(got[b, h][kk].double().cpu().numpy() - r) / np.linalg.norm(r)
+                assert rel <= 1e-2, (name, b, h, rel)
+            print(f"  key rows of head ({b},{h}) checked", flush=True)
