@@ -92,25 +92,27 @@ def _block_backward(qb, K, V, dOb, s):
 
 
 def forward_backward(q, k, v, dout, scale, block=QUERY_BLOCK, heads=None):
-    """Full fp64 forward and backward. Returns a dict with o, lse, D, dq, dk,
-    dv over all (b, h), or only over the (b, h) pairs listed in `heads`
-    (other entries are left as NaN)."""
+    """Full fp64 forward and backward. Returns a dict with o, lse, D, dq (one
+    row per query) and dk, dv (one row per key; the key count may differ
+    from the query count) over all (b, h), or only over the (b, h) pairs
+    listed in `heads` (other entries are left as NaN)."""
     q, k, v, dout = _as_f64(q), _as_f64(k), _as_f64(v), _as_f64(dout)
     s = fp32_scale(scale)
     B, H, N, d = q.shape
+    Nk = k.shape[2]
     out = {
         "o": np.full((B, H, N, d), np.nan),
         "lse": np.full((B, H, N), np.nan),
         "D": np.full((B, H, N), np.nan),
         "dq": np.full((B, H, N, d), np.nan),
-        "dk": np.full((B, H, N, d), np.nan),
-        "dv": np.full((B, H, N, d), np.nan),
+        "dk": np.full((B, H, Nk, d), np.nan),
+        "dv": np.full((B, H, Nk, d), np.nan),
     }
     pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(H)]
     for b, h in pairs:
         K, V = k[b, h], v[b, h]
-        dk = np.zeros((N, d))
-        dv = np.zeros((N, d))
+        dk = np.zeros((Nk, d))
+        dv = np.zeros((Nk, d))
         for r0 in range(0, N, block):
             r1 = min(N, r0 + block)
             r = _block_backward(q[b, h, r0:r1], K, V, dout[b, h, r0:r1], s)

@@ -300,9 +300,14 @@ def test_row_statistics_and_key_rows_with_other_key_counts(Nq, Nk):
                                atol=1e-14)
     keys = np.array([0, 11, Nk - 1])
     dk, dv = oracle.key_rows(q, k, v, dout, s, 0, 1, keys, lse, D, block=16)
-    _, dk_full, dv_full = segment_backward(q, k, v, dout, o, lse_f, s)
+    dq_full, dk_full, dv_full = segment_backward(q, k, v, dout, o, lse_f, s)
     np.testing.assert_allclose(dk, dk_full[0, 1, keys], rtol=1e-11, atol=1e-13)
     np.testing.assert_allclose(dv, dv_full[0, 1, keys], rtol=1e-11, atol=1e-13)
+    # the full pass at these lengths: one dK, dV row per key
+    full = oracle.forward_backward(q, k, v, dout, s, block=16)
+    assert full["dk"].shape == (1, 2, Nk, 8) and full["dq"].shape == (1, 2, Nq, 8)
+    for name, ref in (("o", o), ("lse", lse_f), ("dq", dq_full), ("dk", dk_full), ("dv", dv_full)):
+        np.testing.assert_allclose(full[name], ref, rtol=1e-11, atol=1e-13)
 
 
 def test_row_ranges_sum_to_full_pass():
