@@ -1,5 +1,6 @@
 """Host-side argument checks of the Python binding: tensors that are not on
-a GPU are rejected with TypeError before any library call."""
+a GPU are rejected with TypeError before any library call, and without the
+built library every call raises (there is no fallback)."""
 import pytest
 
 torch = pytest.importorskip("torch")
@@ -44,3 +45,18 @@ def test_other_rows_reject_host_tensors():
         va.agg_fwd(bf16(2, 64), bf16(3, 2, 5, 64), bf16(3, 2, 5, 64))
     with pytest.raises(TypeError):
         va.ulysses_pack(bf16(1, 8, 4, 64), 2)
+
+
+def test_missing_library_raises_instead_of_falling_back(monkeypatch):
+    # there is no CPU or PyTorch path: without the built library every call
+    # that needs it raises
+    from paper_2405_15780_amd import binding
+
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", "/nonexistent/libvitattn.so")
+    with pytest.raises(ImportError, match="is missing"):
+        binding.library()
+    with pytest.raises(ImportError, match="is missing"):
+        binding.workspace_bytes(1, 1, 8, 64)
+    with pytest.raises(ImportError, match="is missing"):
+        binding.version()
